@@ -1,0 +1,231 @@
+#!/usr/bin/env python3
+"""Throughput of the delta-extraction hot path on one MI355X.
+
+One step = one pass of the whole path over the trainer shard already
+resident in HBM: reset the delta cursor, dte_extract_delta (AdamW
+inversion + BF16 change detection + compaction), dte_remap (receiver
+coordinates) and dte_apply (scatter into the receiver BF16 shards).
+
+Default workload: the full Qwen3-8B state (8,190,735,360 fp32 elements of
+theta, m, v; receiver TP=4).  Prints one JSON line with the throughput in
+elements/s, the roofline of the dominant kernel (extract, HBM-bound) and
+the CPU oracle's throughput on a bounded sample of the same workload.
+
+Other workloads (--workload): tiny_block_tp2, qwen3_30b_a3b_12l_ep8,
+qwen3_8b_4l_tp4 (with --lr), qwen3_8b_tp8_apply (apply-only timing of the
+Qwen3-8B delta into eight TP=8 shards).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def workload(name, lr):
+    import synth
+    from synth import workloads as W
+    if name == "qwen3_8b_tp4":
+        return W.qwen3_8b(4)
+    if name == "qwen3_8b_tp8_apply":
+        return W.qwen3_8b(8)
+    if name == "tiny_block_tp2":
+        return W.tiny_block()
+    if name == "qwen3_30b_a3b_12l_ep8":
+        return W.qwen3_30b_a3b_share(synth.word)
+    if name == "qwen3_8b_4l_tp4":
+        return W.qwen3_8b_layers_sweep(lr if lr is not None else 1e-6)
+    raise SystemExit("unknown workload %r" % name)
+
+
+def cpu_baseline(seconds_target=15.0):
+    """The oracle (O3-O8: inversion, BF16 detection, nonzero, remap, apply)
+    timed on host cores over a bounded sample: whole Qwen3-8B layers (the
+    tensors of the default workload), each layer's state generated untimed."""
+    import numpy as np
+
+    import synth
+    from oracle import core, plan, remap, run
+    from synth import workloads as W
+
+    threads = synth.default_threads()
+    wl = W.qwen3_8b_layers_sweep(1e-6, layers=1)
+    pl = plan.build_plan(wl)
+    sc = core.derive_scalars(wl.hp)
+    wins = run.windows(wl, 1 << 22)
+    elems, secs, layers = 0, 0.0, 0
+    from concurrent.futures import ThreadPoolExecutor
+    while secs < seconds_target and layers < 8:
+        states = []
+        with ThreadPoolExecutor(threads) as ex:
+            states = list(ex.map(lambda w: run.state(wl, w.tensor, w.lo, w.hi, sc), wins))
+        shards = [np.zeros(n, np.uint16) for n in pl.rank_numel]
+        begins = wl.flat_begins()
+        t0 = time.perf_counter()
+        with ThreadPoolExecutor(threads) as ex:
+            parts = list(ex.map(
+                lambda a: core.detect(a[1][1], a[1][2], a[1][3], sc,
+                                      begins[a[0].tensor] + a[0].lo)[:2],
+                zip(wins, states)))
+        idx = np.concatenate([x[0] for x in parts])
+        val = np.concatenate([x[1] for x in parts])
+        remap.apply(shards, remap.remap(pl, idx, val))
+        secs += time.perf_counter() - t0
+        elems += wl.numel
+        layers += 1
+        del states
+    return {"value": elems / secs, "unit": "elements/s", "cores": threads, "kind": "oracle",
+            "sample": "%d x one Qwen3-8B layer (%d elements each, receiver TP=4): "
+                      "inversion+BF16 detection+nonzero+remap+apply, state generation "
+                      "untimed; %s" % (layers, wl.numel, run.host_description()),
+            "seconds": secs}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen3_8b_tp4")
+    ap.add_argument("--lr", type=float, default=None)
+    ap.add_argument("--capacity-fraction", type=float, default=0.02)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2608_00455_amd import layouts
+    from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state
+
+    torch.cuda.set_device(0)
+    wl = workload(args.workload, args.lr)
+    hp = wl.hp if args.lr is None else type(wl.hp)(lr=args.lr)
+    n = wl.numel
+    log("bench: workload %s, %d elements, lr %g" % (wl.name, n, hp.lr))
+    t = time.perf_counter()
+    p, m, v = generate_state(wl, hp)
+    log("bench: state generated in %.1f s" % (time.perf_counter() - t))
+    spec = layouts.build_spec(wl)
+    cap = max(1 << 20, int(n * args.capacity_fraction))
+    pipe = DeltaPipeline(spec, capacity=cap)
+    stream = torch.cuda.current_stream()
+    apply_only = args.workload.endswith("_apply")
+
+    def step(ev=None):
+        if apply_only:
+            if ev:
+                ev[0].record(stream)
+            pipe.apply()
+            if ev:
+                ev[1].record(stream)
+            return
+        pipe.reset()
+        if ev:
+            ev[0].record(stream)
+        pipe.extract(p, m, v, hp)
+        if ev:
+            ev[1].record(stream)
+        pipe.remap()
+        if ev:
+            ev[2].record(stream)
+        pipe.apply()
+        if ev:
+            ev[3].record(stream)
+
+    if apply_only:                           # delta and buckets prepared untimed
+        pipe.step(p, m, v, hp)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    nev = 2 if apply_only else 4
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_step = total_ms / args.steps
+    changed = int(pipe.cursor.item())
+    counts = pipe.rank_count.cpu().tolist()
+    routed = int(sum(counts))
+    if changed > cap or any(c > cap for c in counts):
+        log("bench: capacity exceeded (changed %d, capacity %d)" % (changed, cap))
+        return 3
+    c = changed / n
+
+    if apply_only:
+        k_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+        k_bytes = routed * (8 + 2 + 2)       # read offset + value, write value
+        value = routed / (ms_step / 1e3)
+        metric_unit = "entries/s"
+        kernel = "apply"
+    else:
+        ext_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+        rem_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+        app_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+        k_ms = ext_ms
+        k_bytes = 12 * n + 10 * changed       # read theta, m, v; write (idx, val)
+        value = n / (ms_step / 1e3)
+        metric_unit = "elements/s"
+        kernel = "extract"
+    step_bytes = (k_bytes if apply_only else
+                  12 * n + 10 * changed + 10 * changed + 10 * routed + 12 * routed)
+    achieved = k_bytes / (k_ms / 1e3) / 1e9
+    out = {
+        "metric": "delta-extract+remap+apply: elements/s and HBM GB/s (% of peak), "
+                  "Qwen3-8B shape",
+        "value": value,
+        "unit": metric_unit,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
+        "config": {"workload": wl.name, "elements": n, "changed": changed,
+                   "change_fraction": c, "receiver_ranks": len(counts),
+                   "routed_entries": routed, "lr": hp.lr,
+                   "step_algorithmic_bytes": step_bytes,
+                   "step_gbs": step_bytes / (ms_step / 1e3) / 1e9,
+                   "step_frac_of_hbm_peak": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS},
+        "roofline": {"kernel": kernel, "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "kernel_ms": k_ms, "bytes_per_launch": k_bytes},
+    }
+    if not apply_only:
+        out["config"].update({"extract_ms": ext_ms, "remap_ms": rem_ms, "apply_ms": app_ms})
+    del p, m, v
+    pipe.close()
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

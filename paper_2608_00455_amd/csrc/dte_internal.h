@@ -1,0 +1,95 @@
+// Internal declarations shared by the host API (dte_api.hip) and the kernel
+// translation units (extract.hip, remap.hip).  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/dte.h"
+
+namespace dte {
+
+// ---- extract (fused AdamW inverse + BF16 detection + compaction) --------
+
+struct ExtractParams {
+    const float* p;
+    const float* m;
+    const float* v;
+    int64_t n;            // elements of this launch
+    int64_t index_base;   // flat trainer offset of element 0
+    float lrb1, rbc2, eps, decay;
+    int64_t* out_idx;
+    uint16_t* out_val;
+    int64_t capacity;
+    int64_t* cursor;
+    float* out_prev;      // nullable
+};
+
+hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream);
+
+struct ForwardParams {
+    float* p;
+    float* m;
+    float* v;
+    const float* g;
+    int64_t n;
+    float lrb1, rbc2, eps, decay, b1, b2, omb1, omb2;
+};
+
+hipError_t launch_adamw_forward(const ForwardParams& a, int cus, hipStream_t stream);
+
+// ---- transfer plan on the device ----------------------------------------
+
+constexpr int kRanksPerLaunch = 16;   // per-rank pointers travel as kernel arguments
+
+struct DevOp {
+    int64_t dst_base;
+    int32_t rank;
+    int32_t ndim;
+    uint32_t src_origin[DTE_MAX_DIMS];
+    uint32_t extent[DTE_MAX_DIMS];
+    uint32_t dst_origin[DTE_MAX_DIMS];
+    uint32_t dst_shape[DTE_MAX_DIMS];
+};
+
+struct PlanView {
+    const int64_t* seg_begin;   // nseg + 1 (last = total)
+    const uint32_t* seg_shape;  // nseg * DTE_MAX_DIMS
+    const int32_t* seg_ndim;    // nseg
+    const int32_t* seg_ops;     // nseg + 1, CSR into ops (by segment)
+    const DevOp* ops;           // nop
+    const int32_t* lookup;      // nbuckets: segment holding element (b << shift)
+    int64_t total;
+    int64_t nbuckets;
+    int32_t nseg;
+    int32_t shift;
+};
+
+struct RankSlice {                 // ranks [first, first + count) of one launch
+    int32_t first;
+    int32_t count;
+    int64_t* off[kRanksPerLaunch];
+    uint16_t* val[kRanksPerLaunch];
+    int64_t cap[kRanksPerLaunch];
+};
+
+hipError_t launch_zero_i64(int64_t* p, int64_t n, hipStream_t stream);
+
+hipError_t launch_remap(const PlanView& plan, const int64_t* idx, const uint16_t* val,
+                        const int64_t* count, int64_t in_capacity, const RankSlice& out,
+                        int64_t* rank_count, int cus, hipStream_t stream);
+
+struct ApplySlice {
+    int32_t first;
+    int32_t count;
+    uint16_t* shard[kRanksPerLaunch];
+    const int64_t* off[kRanksPerLaunch];
+    const uint16_t* val[kRanksPerLaunch];
+    int64_t cap[kRanksPerLaunch];
+    int64_t numel[kRanksPerLaunch];
+};
+
+hipError_t launch_apply(const ApplySlice& s, const int64_t* rank_count, int cus,
+                        hipStream_t stream);
+
+}  // namespace dte

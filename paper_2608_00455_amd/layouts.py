@@ -1,0 +1,228 @@
+"""Transfer-plan construction for the receiver layouts (paper sec. 3.2.2:
+the plan T is precomputed from sender and receiver shard metadata;
+Observation 3: the layouts fix it before synchronisation).
+
+Host-side metadata only: the result is handed to dte_plan_create, which
+validates it (coverage, bounds, single writer per receiver element).
+
+Sender side: the flat trainer shard holds the canonical (Hugging Face)
+tensors back to back in parameter order; each is one dte_segment.
+Receiver side, per rank, a flat BF16 buffer of consecutive tensors:
+  dense, tensor parallel degree P (rank r):
+    embed_tokens / lm_head  rows [r V/P, (r+1) V/P)
+    per layer: input_layernorm (whole), qkv_proj = [q_r; k_r; v_r] (row
+    slices), q_norm, k_norm (whole), o_proj columns [r qd/P, ...),
+    post_attention_layernorm (whole), gate_up_proj = [gate_r; up_r] (row
+    slices), down_proj columns [r I/P, ...); then norm (whole), lm_head.
+  MoE, R ranks, attention TP degree A, E experts per rank (rank r):
+    per layer: input_layernorm, attention block as above on shard r % A,
+    post_attention_layernorm, router (whole), w13 [E, 2I, h] with expert
+    e = r E + s in slot s as [gate_e; up_e], w2 [E, h, I] with down_e.
+An expert slot of w13 / w2 is addressed as its own 2-D view at the slot's
+flat offset, so every plan operation has the rank of its canonical tensor.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Tuple
+
+from .binding import DTE_MAX_DIMS, dte_op, dte_segment
+
+
+@dataclass
+class Piece:
+    segment: int
+    src_lo: Tuple[int, ...]
+    extent: Tuple[int, ...]
+    dst_lo: Tuple[int, ...]
+
+
+@dataclass
+class View:
+    name: str
+    shape: Tuple[int, ...]
+    pieces: List[Piece] = field(default_factory=list)
+
+
+@dataclass
+class PlanSpec:
+    segments: List[Tuple[int, Tuple[int, ...]]]      # (flat_begin, shape)
+    views: List[List[Tuple[int, View]]]               # per rank: (flat base, view)
+    rank_numel: List[int]
+
+    @property
+    def nranks(self) -> int:
+        return len(self.rank_numel)
+
+    @property
+    def total(self) -> int:
+        b, s = self.segments[-1]
+        n = 1
+        for x in s:
+            n *= x
+        return b + n
+
+    def c_segments(self) -> List[dte_segment]:
+        out = []
+        for begin, shape in self.segments:
+            sg = dte_segment()
+            sg.flat_begin = begin
+            sg.ndim = len(shape)
+            for d in range(DTE_MAX_DIMS):
+                sg.shape[d] = shape[d] if d < len(shape) else 1
+            out.append(sg)
+        return out
+
+    def c_ops(self) -> List[dte_op]:
+        ops = []
+        for rank, views in enumerate(self.views):
+            for base, vw in views:
+                for pc in vw.pieces:
+                    o = dte_op()
+                    o.segment = pc.segment
+                    o.rank = rank
+                    o.dst_base = base
+                    nd = len(vw.shape)
+                    for d in range(DTE_MAX_DIMS):
+                        o.src_origin[d] = pc.src_lo[d] if d < nd else 0
+                        o.extent[d] = pc.extent[d] if d < nd else 1
+                        o.dst_origin[d] = pc.dst_lo[d] if d < nd else 0
+                        o.dst_shape[d] = vw.shape[d] if d < nd else 1
+                    ops.append(o)
+        return ops
+
+
+def _part(total: int, parts: int, i: int) -> Tuple[int, int]:
+    if total % parts:
+        raise ValueError("%d does not split evenly into %d parts" % (total, parts))
+    w = total // parts
+    return i * w, w
+
+
+class _Index:
+    """Segment lookup by (layer, role, expert)."""
+
+    def __init__(self, wl):
+        self.wl = wl
+        self.key: Dict[Tuple, int] = {}
+        for k, t in enumerate(wl.tensors):
+            self.key[(t.layer, t.role, t.expert)] = k
+        self.layers = sorted({t.layer for t in wl.tensors if t.layer is not None})
+
+    def seg(self, layer, role, expert=None):
+        return self.key.get((layer, role, expert))
+
+    def shape(self, k):
+        return tuple(self.wl.tensors[k].shape)
+
+
+def _whole(ix, k, name):
+    s = ix.shape(k)
+    return View(name, s, [Piece(k, (0,) * len(s), s, (0,) * len(s))])
+
+
+def _stack_rows(ix, name, parts):
+    """View made of row slices [lo, lo+cnt) of 2-D segments, stacked in order."""
+    cols = ix.shape(parts[0][0])[1]
+    rows, pieces = 0, []
+    for k, lo, cnt in parts:
+        assert ix.shape(k)[1] == cols
+        pieces.append(Piece(k, (lo, 0), (cnt, cols), (rows, 0)))
+        rows += cnt
+    return View(name, (rows, cols), pieces)
+
+
+def _col_slice(ix, name, k, lo, cnt):
+    rows = ix.shape(k)[0]
+    return View(name, (rows, cnt), [Piece(k, (0, lo), (rows, cnt), (0, 0))])
+
+
+def _attention_views(ix, L, P, a, pre):
+    q, k, v, o = (ix.seg(L, r) for r in ("q", "k", "v", "o"))
+    qlo, qn = _part(ix.shape(q)[0], P, a)
+    klo, kn = _part(ix.shape(k)[0], P, a)
+    views = [_stack_rows(ix, pre + "qkv_proj", [(q, qlo, qn), (k, klo, kn), (v, klo, kn)])]
+    for role, nm in (("q_norm", "q_norm"), ("k_norm", "k_norm")):
+        s = ix.seg(L, role)
+        if s is not None:
+            views.append(_whole(ix, s, pre + nm))
+    olo, on = _part(ix.shape(o)[1], P, a)
+    views.append(_col_slice(ix, pre + "o_proj", o, olo, on))
+    return views
+
+
+def _dense_rank(ix, r, P):
+    views = []
+    emb = ix.seg(None, "embed")
+    if emb is not None:
+        lo, n = _part(ix.shape(emb)[0], P, r)
+        views.append(_stack_rows(ix, "embed_tokens", [(emb, lo, n)]))
+    for L in ix.layers:
+        pre = "layers.%d." % L
+        views.append(_whole(ix, ix.seg(L, "in_norm"), pre + "input_layernorm"))
+        views += _attention_views(ix, L, P, r, pre)
+        views.append(_whole(ix, ix.seg(L, "post_norm"), pre + "post_attention_layernorm"))
+        g, u, d = ix.seg(L, "gate"), ix.seg(L, "up"), ix.seg(L, "down")
+        lo, n = _part(ix.shape(g)[0], P, r)
+        views.append(_stack_rows(ix, pre + "gate_up_proj", [(g, lo, n), (u, lo, n)]))
+        dlo, dn = _part(ix.shape(d)[1], P, r)
+        views.append(_col_slice(ix, pre + "down_proj", d, dlo, dn))
+    fn = ix.seg(None, "final_norm")
+    if fn is not None:
+        views.append(_whole(ix, fn, "norm"))
+    head = ix.seg(None, "lm_head")
+    if head is not None:
+        lo, n = _part(ix.shape(head)[0], P, r)
+        views.append(_stack_rows(ix, "lm_head", [(head, lo, n)]))
+    return views
+
+
+def _moe_rank(ix, r, R, A, E):
+    views = []
+    for L in ix.layers:
+        pre = "layers.%d." % L
+        views.append(_whole(ix, ix.seg(L, "in_norm"), pre + "input_layernorm"))
+        views += _attention_views(ix, L, A, r % A, pre)
+        views.append(_whole(ix, ix.seg(L, "post_norm"), pre + "post_attention_layernorm"))
+        views.append(_whole(ix, ix.seg(L, "router"), pre + "router"))
+        for slot in range(E):                       # w13 slots, then w2 slots
+            e = r * E + slot
+            g, u = ix.seg(L, "expert_gate", e), ix.seg(L, "expert_up", e)
+            ie = ix.shape(g)[0]
+            views.append(_stack_rows(ix, pre + "w13[%d]" % slot, [(g, 0, ie), (u, 0, ie)]))
+        for slot in range(E):
+            e = r * E + slot
+            views.append(_whole(ix, ix.seg(L, "expert_down", e), pre + "w2[%d]" % slot))
+    return views
+
+
+def build_spec(wl) -> PlanSpec:
+    ix = _Index(wl)
+    segments, pos = [], 0
+    for t in wl.tensors:
+        segments.append((pos, tuple(t.shape)))
+        pos += t.numel
+    rc = wl.receiver
+    per_rank = []
+    for r in range(rc.nranks):
+        if rc.kind == "tp":
+            vs = _dense_rank(ix, r, rc.tp)
+        elif rc.kind == "moe_ep":
+            if rc.ranks % rc.attn_tp:
+                raise ValueError("ranks must be a multiple of the attention TP degree")
+            vs = _moe_rank(ix, r, rc.ranks, rc.attn_tp, rc.experts_per_rank)
+        else:
+            raise ValueError("unknown receiver layout %r" % rc.kind)
+        per_rank.append(vs)
+    placed, numel = [], []
+    for vs in per_rank:
+        base, lst = 0, []
+        for vw in vs:
+            lst.append((base, vw))
+            n = 1
+            for x in vw.shape:
+                n *= x
+            base += n
+        placed.append(lst)
+        numel.append(base)
+    return PlanSpec(segments, placed, numel)

@@ -1,0 +1,167 @@
+"""Device buffers and call sequencing for the three hot calls.
+
+torch is used for device memory and streams only; every step of the path
+runs inside libdte.so.  `DeltaPipeline` owns the delta buffers (I, V and
+the cursor), the per-receiver buckets and counts, and the receiver shards,
+and chains dte_extract_delta -> dte_remap -> dte_apply on one stream.
+`generate_state` produces a synthetic post-step trainer state on the device
+(seeded draws from `synth`, then the library's AdamW step).
+"""
+from __future__ import annotations
+
+from typing import List, Optional
+
+import torch
+
+from . import binding as B
+from .layouts import PlanSpec, build_spec
+
+
+def _stream(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class Plan:
+    """Owned dte_plan handle."""
+
+    def __init__(self, spec: PlanSpec):
+        self.spec = spec
+        self.handle = B.dte_plan_create(spec.c_segments(), spec.c_ops(), spec.nranks,
+                                        spec.rank_numel)
+        self.total, self.nranks, self.max_replication = B.dte_plan_info(self.handle)
+
+    def close(self):
+        if self.handle:
+            B.dte_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):  # pragma: no cover - interpreter shutdown order
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class DeltaPipeline:
+    def __init__(self, spec: PlanSpec, capacity: int, rank_capacity: Optional[List[int]] = None,
+                 device="cuda", shards: Optional[List[torch.Tensor]] = None):
+        self.plan = Plan(spec)
+        self.device = torch.device(device)
+        self.capacity = int(capacity)
+        R = self.plan.nranks
+        rc = rank_capacity or [self.capacity] * R
+        self.rank_capacity = [int(x) for x in rc]
+        self.idx = torch.empty(max(1, self.capacity), dtype=torch.int64, device=self.device)
+        self.val = torch.empty(max(1, self.capacity), dtype=torch.int16, device=self.device)
+        self.cursor = torch.zeros(1, dtype=torch.int64, device=self.device)
+        self.off = [torch.empty(max(1, c), dtype=torch.int64, device=self.device)
+                    for c in self.rank_capacity]
+        self.rval = [torch.empty(max(1, c), dtype=torch.int16, device=self.device)
+                     for c in self.rank_capacity]
+        self.rank_count = torch.zeros(R, dtype=torch.int64, device=self.device)
+        if shards is None:
+            shards = [torch.zeros(max(1, n), dtype=torch.int16, device=self.device)
+                      for n in spec.rank_numel]
+        self.shards = shards
+
+    # -- the three hot calls ------------------------------------------------
+    def reset(self, stream=None):
+        """Start a fresh delta (cursor = 0); a fill kernel, graph-safe."""
+        with torch.cuda.stream(stream) if stream is not None else _null():
+            self.cursor.zero_()
+
+    def extract(self, p, m, v, hp, n=None, index_base=0, out_prev=None, stream=None):
+        n = p.numel() if n is None else n
+        B.dte_extract_delta(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, index_base, hp,
+                            self.idx.data_ptr(), self.val.data_ptr(), self.capacity,
+                            self.cursor.data_ptr(),
+                            out_prev.data_ptr() if out_prev is not None else 0, _stream(stream))
+
+    def remap(self, stream=None):
+        B.dte_remap(self.plan.handle, self.idx.data_ptr(), self.val.data_ptr(),
+                    self.cursor.data_ptr(), self.capacity, [t.data_ptr() for t in self.off],
+                    [t.data_ptr() for t in self.rval], self.rank_capacity,
+                    self.rank_count.data_ptr(), _stream(stream))
+
+    def apply(self, stream=None):
+        B.dte_apply(self.plan.handle, [t.data_ptr() for t in self.shards],
+                    [t.data_ptr() for t in self.off], [t.data_ptr() for t in self.rval],
+                    self.rank_count.data_ptr(), self.rank_capacity, _stream(stream))
+
+    def step(self, p, m, v, hp, stream=None):
+        self.reset(stream)
+        self.extract(p, m, v, hp, stream=stream)
+        self.remap(stream)
+        self.apply(stream)
+
+    # -- host read-back (tests) --------------------------------------------
+    def delta(self):
+        """(idx, val) on the host, sorted by idx; and the cursor value."""
+        total = int(self.cursor.item())
+        k = min(total, self.capacity)
+        idx = self.idx[:k].cpu().numpy()
+        val = self.val[:k].cpu().numpy().view("uint16")
+        order = idx.argsort(kind="stable")
+        return idx[order], val[order], total
+
+    def buckets(self):
+        counts = self.rank_count.cpu().numpy()
+        out = []
+        for r in range(self.plan.nranks):
+            k = min(int(counts[r]), self.rank_capacity[r])
+            off = self.off[r][:k].cpu().numpy()
+            val = self.rval[r][:k].cpu().numpy().view("uint16")
+            order = off.argsort(kind="stable")
+            out.append((off[order], val[order]))
+        return out, counts
+
+    def close(self):
+        self.plan.close()
+
+
+class _null:
+    def __enter__(self):
+        return None
+
+    def __exit__(self, *a):
+        return False
+
+
+def generate_state(wl, hp=None, device="cuda"):
+    """Post-step state (p, m, v) of workload `wl` on the device.
+
+    Seeded pre-step draws per tensor (synth), then one dte_adamw_forward
+    over the whole flat shard.  Untouched tensors get zero moments and
+    gradient.  Returns three flat float32 tensors of wl.numel elements.
+    """
+    import synth
+    from synth.workloads import KIND_GRAD, KIND_M_PREV, KIND_P_PREV, KIND_V_PREV
+
+    hp = hp or wl.hp
+    n = wl.numel
+    dev = torch.device(device)
+    p = torch.empty(n, dtype=torch.float32, device=dev)
+    m = torch.empty(n, dtype=torch.float32, device=dev)
+    v = torch.empty(n, dtype=torch.float32, device=dev)
+    g = torch.empty(n, dtype=torch.float32, device=dev)
+    s = torch.cuda.current_stream().cuda_stream
+    for k, (t, begin) in enumerate(zip(wl.tensors, wl.flat_begins())):
+        sl = slice(begin, begin + t.numel)
+        synth.fill_gpu(p[sl].data_ptr(), t.numel, wl.seed, k, KIND_P_PREV, 0, s)
+        if t.touched:
+            synth.fill_gpu(m[sl].data_ptr(), t.numel, wl.seed, k, KIND_M_PREV, 0, s)
+            synth.fill_gpu(v[sl].data_ptr(), t.numel, wl.seed, k, KIND_V_PREV, 0, s)
+            synth.fill_gpu(g[sl].data_ptr(), t.numel, wl.seed, k, KIND_GRAD, 0, s)
+        else:
+            m[sl].zero_()
+            v[sl].zero_()
+            g[sl].zero_()
+    B.dte_adamw_forward(p.data_ptr(), m.data_ptr(), v.data_ptr(), g.data_ptr(), n, hp, s)
+    torch.cuda.current_stream().synchronize()
+    del g
+    return p, m, v
+
+
+def spec_for(wl) -> PlanSpec:
+    return build_spec(wl)

@@ -1,0 +1,297 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Bit-exact: delta index set, BF16 values, reconstructed binary32 weights
+(0 ulp), remapped (rank, offset, value) entries and applied shards; the
+capacity / count semantics; edge cases (empty, ragged, misaligned,
+special values, DECAY != 1, many ranks).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import core as ocore
+from oracle import plan as oplan
+from oracle import remap as oremap
+from oracle import run as orun
+from paper_2608_00455_amd import binding as B
+from paper_2608_00455_amd import layouts
+from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state
+from synth import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host_u16(t):
+    return t.cpu().numpy().view(np.uint16)
+
+
+def sync():
+    torch.cuda.synchronize()
+
+
+def oracle_state(wl, hp=None):
+    res = orun.extract(wl, hp=hp, keep=("p", "m", "v", "ph", "p_prev"))
+    return res, {k: orun.flat(res.parts, k) for k in ("p", "m", "v", "ph", "p_prev")}
+
+
+def assert_delta_equal(pipe, res):
+    idx, val, total = pipe.delta()
+    assert total == res.idx.size
+    assert np.array_equal(idx, res.idx)
+    assert np.array_equal(val, res.val)
+
+
+def test_synth_device_draws_equal_host_draws():
+    say("case: synth fill gpu vs cpu")
+    n = 1_000_003
+    for kind in range(4):
+        g = torch.empty(n, dtype=torch.float32, device="cuda")
+        synth.fill_gpu(g.data_ptr(), n, 4242, 17, kind, 123_456_789)
+        sync()
+        c = synth.draw_cpu(n, 4242, 17, kind, 123_456_789)
+        assert np.array_equal(g.cpu().numpy().view(np.uint32), c.view(np.uint32)), kind
+
+
+def test_forward_step_equals_oracle():
+    wl = W.scaled_moe(synth.word, layers=1, ranks=4, attn_tp=2, experts=8)
+    say("case: adamw forward", wl.name)
+    p, m, v = generate_state(wl)
+    _, st = oracle_state(wl)
+    for name, t in (("p", p), ("m", m), ("v", v)):
+        assert np.array_equal(t.cpu().numpy().view(np.uint32), st[name].view(np.uint32)), name
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    wl = W.tiny_block()
+    res, st = oracle_state(wl)
+    return wl, res, st
+
+
+def test_extract_on_oracle_inputs_tiny_block(tiny):
+    wl, res, st = tiny
+    say("case: extract tiny_block on oracle inputs")
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=wl.numel)
+    p, m, v = dev(st["p"]), dev(st["m"]), dev(st["v"])
+    prev = torch.empty_like(p)
+    pipe.reset()
+    pipe.extract(p, m, v, wl.hp, out_prev=prev)
+    sync()
+    assert_delta_equal(pipe, res)
+    assert np.array_equal(prev.cpu().numpy().view(np.uint32), st["ph"].view(np.uint32))
+    pipe.close()
+
+
+def test_full_path_tiny_block_generated_state(tiny):
+    wl, res, st = tiny
+    say("case: full path tiny_block, device-generated state")
+    p, m, v = generate_state(wl)
+    pl = oplan.build_plan(wl)
+    old = oremap.layout(pl, ocore.bf16(st["ph"]))
+    new = oremap.layout(pl, ocore.bf16(st["p"]))
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=wl.numel // 16, shards=[dev(x.view(np.int16)) for x in old])
+    pipe.step(p, m, v, wl.hp)
+    sync()
+    assert_delta_equal(pipe, res)
+    buckets, counts = pipe.buckets()
+    want = oremap.remap(pl, res.idx, res.val)
+    for r in range(pl.nranks):
+        assert counts[r] == want[r][0].size
+        assert np.array_equal(buckets[r][0], want[r][0])
+        assert np.array_equal(buckets[r][1], want[r][1])
+    for r in range(pl.nranks):
+        assert np.array_equal(host_u16(pipe.shards[r]), new[r]), r
+    # applying the same delta again changes nothing (target values)
+    pipe.apply()
+    sync()
+    for r in range(pl.nranks):
+        assert np.array_equal(host_u16(pipe.shards[r]), new[r]), r
+    pipe.close()
+
+
+@pytest.mark.parametrize("lr", [0.0, 1e-7, 1e-6, 1e-5, 1e-4, 1e-2])
+def test_learning_rates_small_dense(lr):
+    wl = W.scaled_dense(layers=2, tp=2, lr=lr)
+    say("case: lr sweep", wl.name, lr)
+    res, st = oracle_state(wl)
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=wl.numel)
+    p, m, v = dev(st["p"]), dev(st["m"]), dev(st["v"])
+    prev = torch.empty_like(p)
+    pipe.reset()
+    pipe.extract(p, m, v, wl.hp, out_prev=prev)
+    pipe.remap()
+    sync()
+    assert_delta_equal(pipe, res)
+    assert np.array_equal(prev.cpu().numpy().view(np.uint32), st["ph"].view(np.uint32))
+    buckets, counts = pipe.buckets()
+    want = oremap.remap(oplan.build_plan(wl), res.idx, res.val)
+    for r in range(len(want)):
+        assert np.array_equal(buckets[r][0], want[r][0])
+        assert np.array_equal(buckets[r][1], want[r][1])
+    if lr == 0.0:
+        assert res.idx.size == 0
+    pipe.close()
+
+
+def test_ragged_misaligned_and_appended_ranges():
+    wl = W.scaled_dense(layers=1, tp=2, lr=1e-4)
+    say("case: ragged / misaligned / append")
+    res, st = oracle_state(wl)
+    n = 4096 * 3 + 13
+    p, m, v = (st[k][:n] for k in ("p", "m", "v"))
+    want_idx, want_val, want_ph = ocore.detect(p, m, v, ocore.derive_scalars(wl.hp), 0)
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=n)
+    P, M, V = dev(p), dev(m), dev(v)
+    prev = torch.zeros(n + 1, dtype=torch.float32, device="cuda")
+    for cut in (0, 1, 4095, 4097, 6001, n - 1, n):
+        pipe.reset()
+        # [0, cut) from aligned bases; [cut, n) from bases offset by `cut`
+        # elements (odd cut: misaligned, scalar-load path)
+        pipe.extract(P, M, V, wl.hp, n=cut, index_base=0, out_prev=prev)
+        pipe.extract(P[cut:], M[cut:], V[cut:], wl.hp, n=n - cut, index_base=cut,
+                     out_prev=prev[cut:])
+        sync()
+        idx, val, total = pipe.delta()
+        assert total == want_idx.size, cut
+        assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val), cut
+        assert np.array_equal(prev[:n].cpu().numpy().view(np.uint32), want_ph.view(np.uint32))
+    # ragged length on aligned buffers (vector path with a partial last tile)
+    for m_len in (1, 3, 4, 5, 4096, 4099, 8191):
+        pipe.reset()
+        pipe.extract(P, M, V, wl.hp, n=m_len)
+        sync()
+        idx, val, total = pipe.delta()
+        sel = want_idx < m_len
+        assert np.array_equal(idx, want_idx[sel]) and np.array_equal(val, want_val[sel]), m_len
+    pipe.close()
+
+
+def test_special_values():
+    say("case: special values")
+    rng = np.random.default_rng(3)
+    n = 5000
+    p = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    m = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    v = np.abs(rng.standard_normal(n) * 1e-6).astype(np.float32)
+    specials = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 1e-45, -1e-45, 1e-40, 3e38,
+                         -3e38, 1.0, -1.0, 65504.0, 1.17549435e-38], np.float32)
+    k = specials.size
+    for j in range(0, 600, k):
+        p[j:j + k] = specials
+        m[j + 200:j + 200 + k] = specials
+        v[j + 400:j + 400 + k] = specials
+    p[4000:4010] = np.array([0x3F808000, 0x3F807FFF, 0x3F818000, 0x7F7F8000, 0x00008000,
+                             0x80000001, 0x7F800001, 0xFFC00000, 0x007F8000, 0x3FFF8000],
+                            np.uint32).view(np.float32)
+    for lr in (1e-6, 1e-4, 3e-1):
+        hp = W.StepHP(lr=lr)
+        sc = ocore.derive_scalars(hp)
+        want_idx, want_val, want_ph = ocore.detect(p, m, v, sc, 1000)
+        spec = layouts.build_spec(W.scaled_dense(layers=1, tp=2))
+        pipe = DeltaPipeline(spec, capacity=n)
+        prev = torch.empty(n, dtype=torch.float32, device="cuda")
+        pipe.reset()
+        pipe.extract(dev(p), dev(m), dev(v), hp, index_base=1000, out_prev=prev)
+        sync()
+        idx, val, total = pipe.delta()
+        assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val), lr
+        got_ph = prev.cpu().numpy()
+        nan = np.isnan(want_ph)
+        assert np.array_equal(np.isnan(got_ph), nan)
+        assert np.array_equal(got_ph.view(np.uint32)[~nan], want_ph.view(np.uint32)[~nan])
+        pipe.close()
+
+
+def test_capacity_overflow_reports_true_total(tiny):
+    wl, res, st = tiny
+    say("case: capacity overflow")
+    spec = layouts.build_spec(wl)
+    cap = res.idx.size // 3
+    pipe = DeltaPipeline(spec, capacity=cap, rank_capacity=[cap // 2, 7])
+    pipe.step(dev(st["p"]), dev(st["m"]), dev(st["v"]), wl.hp)
+    sync()
+    idx, val, total = pipe.delta()
+    assert total == res.idx.size and idx.size == cap
+    assert np.unique(idx).size == cap
+    pos = np.searchsorted(res.idx, idx)
+    assert np.array_equal(res.idx[pos], idx) and np.array_equal(res.val[pos], val)
+    # buckets: a duplicate-free subset of the oracle's buckets of the full
+    # delta, truncated at each rank's capacity
+    buckets, counts = pipe.buckets()
+    full = oremap.remap(oplan.build_plan(wl), res.idx, res.val)
+    for r in range(2):
+        got_off, got_val = buckets[r]
+        assert got_off.size == min(counts[r], pipe.rank_capacity[r])
+        assert counts[r] <= full[r][0].size
+        assert np.unique(got_off).size == got_off.size
+        pos = np.searchsorted(full[r][0], got_off)
+        assert np.array_equal(full[r][0][pos], got_off)
+        assert np.array_equal(full[r][1][pos], got_val)
+    pipe.close()
+
+
+@pytest.mark.parametrize("make", [
+    lambda: W.tiny_block(),
+    lambda: W.scaled_moe(synth.word, layers=2, ranks=8, attn_tp=2, experts=16, hidden=64,
+                         head_dim=16, expert_intermediate=24),
+    lambda: W.scaled_dense(layers=1, tp=32, heads_q=32, heads_kv=32, head_dim=8, hidden=64,
+                           intermediate=128, vocab=64),
+])
+def test_remap_and_apply_of_every_offset(make):
+    """Remap of idx = arange(N) (every element changed) against the oracle:
+    a bijection onto the receiver shards; apply fills every element."""
+    wl = make()
+    say("case: remap all offsets", wl.name)
+    n = wl.numel
+    pl = oplan.build_plan(wl)
+    idx = np.arange(n, dtype=np.int64)
+    val = (idx * 2654435761 >> 7).astype(np.uint16)
+    want = oremap.remap(pl, idx, val)
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=n)
+    pipe.idx.copy_(dev(idx))
+    pipe.val.copy_(dev(val.view(np.int16)))
+    pipe.cursor.fill_(n)
+    pipe.remap()
+    pipe.apply()
+    sync()
+    buckets, counts = pipe.buckets()
+    for r in range(pl.nranks):
+        assert counts[r] == pl.rank_numel[r]
+        assert np.array_equal(buckets[r][0], np.arange(pl.rank_numel[r]))
+        assert np.array_equal(buckets[r][1], want[r][1])
+        assert np.array_equal(host_u16(pipe.shards[r]), want[r][1])
+    pipe.close()
+
+
+def test_empty_delta_leaves_shards_untouched():
+    wl = W.scaled_dense(layers=1, tp=2, lr=0.0)
+    say("case: empty delta")
+    spec = layouts.build_spec(wl)
+    sentinel = [torch.full((n,), 0x7FFF, dtype=torch.int16, device="cuda")
+                for n in spec.rank_numel]
+    pipe = DeltaPipeline(spec, capacity=1024, shards=sentinel)
+    p, m, v = generate_state(wl)
+    pipe.step(p, m, v, wl.hp)
+    sync()
+    assert pipe.delta()[2] == 0
+    assert int(pipe.rank_count.sum().item()) == 0
+    for s in pipe.shards:
+        assert bool((s == 0x7FFF).all())
+    pipe.close()

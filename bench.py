@@ -92,6 +92,28 @@ def cpu_baseline(seconds_target=15.0):
             "seconds": secs}
 
 
+def copy_calibration(gib):
+    """A plain copy of known size: reads and writes gib GiB once per launch."""
+    import torch
+    n = int(gib * (1 << 30)) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    reps = 5
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "ms": ms,
+                      "gbs_read_plus_write": 8 * n / (ms / 1e3) / 1e9}), flush=True)
+    return 0
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -102,6 +124,9 @@ def main():
     ap.add_argument("--capacity-fraction", type=float, default=0.02)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
+                    help="only time a plain device copy of GIB GiB (for scaling the "
+                         "FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -114,6 +139,8 @@ def main():
     from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state
 
     torch.cuda.set_device(0)
+    if args.copy_calibration > 0:
+        return copy_calibration(args.copy_calibration)
     wl = workload(args.workload, args.lr)
     hp = wl.hp if args.lr is None else type(wl.hp)(lr=args.lr)
     n = wl.numel

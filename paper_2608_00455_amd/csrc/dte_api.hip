@@ -299,6 +299,13 @@ dte_status dte_extract_delta(const float* p, const float* m, const float* v, int
     a.rbc2 = sc.s.rbc2;
     a.eps = sc.s.eps;
     a.decay = sc.s.decay;
+    {
+        // one binary32 step below and above the binary64 reciprocal: a
+        // bracket of 1/decay whatever the binary64 rounding did
+        const float r = (float)(1.0 / (double)sc.s.decay);
+        a.rd_lo = std::nextafter(r, 0.0f);
+        a.rd_hi = std::nextafter(r, INFINITY);
+    }
     a.out_idx = out_idx;
     a.out_val = out_val;
     a.capacity = capacity;

@@ -18,6 +18,7 @@ struct ExtractParams {
     int64_t n;            // elements of this launch
     int64_t index_base;   // flat trainer offset of element 0
     float lrb1, rbc2, eps, decay;
+    float rd_lo, rd_hi;   // binary32 bracket of 1/decay: rd_lo <= 1/decay <= rd_hi
     int64_t* out_idx;
     uint16_t* out_val;
     int64_t capacity;

@@ -295,3 +295,37 @@ def test_empty_delta_leaves_shards_untouched():
     for s in pipe.shards:
         assert bool((s == 0x7FFF).all())
     pipe.close()
+
+
+@pytest.mark.parametrize("lr", [1e-7, 1e-6, 1e-4, 3e-2])
+def test_values_at_bf16_rounding_midpoints(lr):
+    """Weights a few binary32 ulps from BF16 rounding midpoints (where the
+    reconstruction decides the pattern), zeros, subnormals and both signs of
+    the moment: every element parity-checked against the oracle."""
+    say("case: rounding midpoints", lr)
+    rng = np.random.default_rng(11)
+    n = 1 << 18
+    hi = rng.integers(0, 1 << 16, n, dtype=np.uint32)
+    hi = (hi & 0x80FF) | (rng.integers(0x30, 0x42, n, dtype=np.uint32) << 7)  # |p| ~ 1e-7..8
+    low = (0x8000 + rng.integers(-40, 41, n)).astype(np.uint32) & 0xFFFF
+    pbits = (hi << 16) | low
+    pbits[:64] = np.arange(64, dtype=np.uint32)                 # +0 and subnormals
+    pbits[64:128] = np.arange(64, dtype=np.uint32) | 0x80000000  # -0 and negative subnormals
+    p = pbits.view(np.float32)
+    m = (rng.standard_normal(n) * 10.0 ** rng.uniform(-9, -2, n)).astype(np.float32)
+    m[::7] = 0.0
+    m[1::7] = -0.0
+    v = np.abs(rng.standard_normal(n) * 10.0 ** rng.uniform(-12, -4, n)).astype(np.float32)
+    v[::5] = 0.0
+    hp = W.StepHP(lr=lr)
+    want_idx, want_val, _ = ocore.detect(p, m, v, ocore.derive_scalars(hp), 0)
+    assert want_idx.size > 100
+    spec = layouts.build_spec(W.scaled_dense(layers=1, tp=2))
+    pipe = DeltaPipeline(spec, capacity=n)
+    pipe.reset()
+    pipe.extract(dev(p), dev(m), dev(v), hp)
+    sync()
+    idx, val, total = pipe.delta()
+    assert total == want_idx.size
+    assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val)
+    pipe.close()

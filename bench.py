@@ -121,7 +121,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen3_8b_tp4")
     ap.add_argument("--lr", type=float, default=None)
-    ap.add_argument("--capacity-fraction", type=float, default=0.02)
+    ap.add_argument("--capacity-fraction", type=float, default=None,
+                    help="delta buffer size as a fraction of the elements (default 0.02, "
+                         "0.25 for the learning-rate sweep)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
@@ -149,7 +151,10 @@ def main():
     p, m, v = generate_state(wl, hp)
     log("bench: state generated in %.1f s" % (time.perf_counter() - t))
     spec = layouts.build_spec(wl)
-    cap = max(1 << 20, int(n * args.capacity_fraction))
+    frac = args.capacity_fraction
+    if frac is None:
+        frac = 0.25 if args.workload == "qwen3_8b_4l_tp4" else 0.02
+    cap = max(1 << 20, int(n * frac))
     pipe = DeltaPipeline(spec, capacity=cap)
     stream = torch.cuda.current_stream()
     apply_only = args.workload.endswith("_apply")

@@ -5,25 +5,30 @@
 //
 // Design (HBM-bound: 12 bytes read per element, ~10 bytes written per
 // changed element):
-//  - persistent grid; every wave walks its own 1024-element tiles (four
-//    float4 of p, m and v per lane: twelve 16-byte non-temporal loads in
-//    flight per lane);
+//  - persistent grid (3 blocks of 4 waves per CU); each block owns one
+//    contiguous range of 2048-element tiles and its waves take every fourth
+//    tile of it (so entries leave each wave as local, ascending runs);
+//    a wave loads eight float4 of p, m and v per lane, i.e. 24 16-byte
+//    non-temporal loads in flight per lane, which is what keeps the HBM
+//    queues full at this occupancy;
 //  - proof of "unchanged" before exact arithmetic: with DECAY == 1 the
 //    reconstruction is ph = RN(p + u), where u has the sign of m and
-//    |u| <= B, B computed from the hardware square root and reciprocal
-//    (about 1 ulp each) and inflated by 2^-16; RN and BF16 rounding are
+//    |u| <= B; B comes from the hardware square root and reciprocal (about
+//    1 ulp each), inflated by 2^-16, plus 2^-126; RN and BF16 rounding are
 //    monotone, so if RN(p + sign(m) B) has the BF16 pattern of p, so has ph.
 //    (DECAY != 1: the same interval is pushed through the division with
-//    bracketing reciprocals of DECAY.)  Only lanes without that proof run the
-//    correctly rounded sqrt / divide of the exact inverse; the result is
-//    bit-identical to evaluating every element exactly.  When theta_hat is
-//    requested every element takes the exact path;
-//  - each element slot's change predicate is a wave64 ballot; a lane's
-//    staging slot is the popcount of the earlier ballots plus mbcnt in its
-//    own; changed entries are staged per wave in LDS (1024 entries) and a
+//    bracketing reciprocals of DECAY.)  Lanes without that proof
+//    (candidates, about as many as the changed elements) queue
+//    (p, m, v, position) in LDS; a wave evaluates 64 queued candidates at a
+//    time with the correctly rounded inverse.  The result is bit-identical
+//    to evaluating every element exactly.  When theta_hat is requested every
+//    element takes the exact path;
+//  - the change predicate of 64 elements is one ballot; a lane's staging
+//    slot is the running count plus mbcnt within the ballot; changed entries
+//    (packed 32-bit position + BF16 value) are staged per wave in LDS and a
 //    wave reserves global output space with one atomicAdd on the 64-bit
-//    cursor per flush of its staging area, then copies the entries out
-//    coalesced.  No block-wide barrier in the main loop.  The number of
+//    cursor per flush of its staging area (1024 entries), then writes the
+//    entries out coalesced.  No block-wide barrier anywhere; the number of
 //    atomics is bounded by entries / 1024 + waves.
 #include <hip/hip_runtime.h>
 
@@ -36,11 +41,12 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / 64;
-constexpr int kVec = 4;                       // float4 per lane per array per tile
+constexpr int kVec = 8;                       // float4 per lane per array per tile
 constexpr int kSlots = 4 * kVec;              // elements per lane per tile
 constexpr int kWaveTile = 64 * kSlots;        // 1024 elements per wave tile
-constexpr int kWaveStage = kWaveTile;         // staging entries per wave (>= one tile)
-constexpr int kBlocksPerCU = 4;               // 40 KB LDS each
+constexpr int kWaveStage = 1024;              // staged output entries per wave (6 bytes each)
+constexpr int kQueue = 128;                   // queued candidates per wave (16 bytes each)
+constexpr int kBlocksPerCU = 3;               // 3 waves per SIMD (VGPR-bound), 32 KB LDS
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -62,13 +68,6 @@ __device__ __forceinline__ uint32_t bf16_bits(float x)
     const uint32_t u = __float_as_uint(x);
     const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
     return (x != x) ? 0x7FC0u : r;
-}
-
-// Same rounding without the NaN rule (used where NaN is excluded).
-__device__ __forceinline__ uint32_t bf16_raw(float x)
-{
-    const uint32_t u = __float_as_uint(x);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
 __device__ __forceinline__ int lane_prefix(uint64_t mask)
@@ -104,20 +103,20 @@ __device__ __forceinline__ bool proven_unchanged(float p, float m, float v, cons
     const float num = a.lrb1 * m;
     const float vh = v * a.rbc2;
     const float den = __builtin_amdgcn_sqrtf(vh) + a.eps;
-    const float bound = __builtin_fabsf(num) * __builtin_amdgcn_rcpf(den) * 1.0000153f;
-    const bool finite = bound < __builtin_inff();           // false for NaN
-    const float b = __builtin_fmaxf(bound, 0x1p-126f);
-    const float lo = p + __builtin_copysignf(0.0f, m);      // RN(p + u) for u = +-0
-    const float hi = p + __builtin_copysignf(b, m);         // RN(p + u) for |u| = B
-    const uint32_t bp = bf16_raw(p);
-    if (kDecayOne)
-        return finite && (p == p) && bf16_raw(lo) == bp && bf16_raw(hi) == bp;
-    // ph = RN(n / DECAY), monotone in n; bracket 1/DECAY by rd_lo <= 1/DECAY <= rd_hi
-    const float x0 = lo * a.rd_lo, x1 = lo * a.rd_hi, x2 = hi * a.rd_lo, x3 = hi * a.rd_hi;
+    const float q = __builtin_fabsf(num) * __builtin_amdgcn_rcpf(den);
+    const float b = __builtin_fmaf(q, 1.0000153f, 0x1p-126f);   // NaN stays NaN
+    const float hi = p + __builtin_copysignf(b, m);
+    const uint32_t up = __float_as_uint(p), uh = __float_as_uint(hi);
+    const uint32_t rp = up + 0x7FFFu + ((up >> 16) & 1u);
+    const uint32_t rh = uh + 0x7FFFu + ((uh >> 16) & 1u);
+    if (kDecayOne) return (rp ^ rh) < 0x10000u;
+    const float x0 = p * a.rd_lo, x1 = p * a.rd_hi, x2 = hi * a.rd_lo, x3 = hi * a.rd_hi;
     const float mn = __builtin_fminf(__builtin_fminf(x0, x1), __builtin_fminf(x2, x3));
     const float mx = __builtin_fmaxf(__builtin_fmaxf(x0, x1), __builtin_fmaxf(x2, x3));
-    return finite && (p == p) && (mn == mn) && (mx == mx) && bf16_raw(mn) == bp &&
-           bf16_raw(mx) == bp;
+    const uint32_t un = __float_as_uint(mn), ux = __float_as_uint(mx);
+    const uint32_t rn = un + 0x7FFFu + ((un >> 16) & 1u);
+    const uint32_t rx = ux + 0x7FFFu + ((ux >> 16) & 1u);
+    return (rp ^ rn) < 0x10000u && (rp ^ rx) < 0x10000u && (mn == mn) && (mx == mx) && (hi == hi);
 }
 
 // Exact inverse and change test of one element (sec. 3.1 / 3.2.1).
@@ -129,18 +128,32 @@ __device__ __forceinline__ float exact_prev(float p, float m, float v, const Ext
     return kDecayOne ? num : num / a.decay;
 }
 
+constexpr int kTileBits = __builtin_ctz(kWaveTile);
+static_assert((1 << kTileBits) == kWaveTile, "wave tile must be a power of two");
+// Per-wave LDS areas.  Keys are (wave iteration << kTileBits) | element in
+// the tile; the wave's tiles are t_first + iteration * nwaves.
 struct WaveStage {
-    int64_t* idx;     // this wave's kWaveStage entries in LDS
+    uint32_t* key;    // output staging: changed entries awaiting a flush
     uint16_t* val;
+    float* qp;        // candidate queue: elements without an "unchanged" proof
+    float* qm;
+    float* qv;
+    uint32_t* qkey;
+    int64_t t_first;
+    int64_t nwaves;
 };
+
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 // Copy a wave's `staged` LDS entries to the reserved global range.
 __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, int staged, int lane)
 {
-    // make every lane's LDS stores visible to the other lanes of the wave
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    wave_sync();   // every lane's LDS stores visible to the other lanes
     unsigned long long base = 0;
     if (lane == 0)
         base = atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor),
@@ -149,27 +162,71 @@ __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, int stag
     for (int i = lane; i < staged; i += 64) {
         const int64_t pos = (int64_t)base + i;
         if (pos < a.capacity) {
-            a.out_idx[pos] = st.idx[i];
+            const uint32_t key = st.key[i];
+            const int64_t t = st.t_first + (int64_t)(key >> kTileBits) * st.nwaves;
+            a.out_idx[pos] = a.index_base + t * kWaveTile + (key & (kWaveTile - 1));
             a.out_val[pos] = st.val[i];
         }
     }
-    // the staging area is rewritten next: finish these reads first
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    wave_sync();   // the staging area is rewritten next: finish these reads first
+}
+
+// Stage one ballot of changed entries (at most 64), flushing first when the
+// staging area would overflow.  Wave-uniform control flow.
+__device__ __forceinline__ void stage_changed(const ExtractParams& a, const WaveStage& st,
+                                              int& staged, int lane, bool changed,
+                                              uint32_t key, uint16_t val)
+{
+    const uint64_t k = __ballot(changed);
+    if (k == 0) return;
+    const int cnt = __popcll(k);
+    if (staged + cnt > kWaveStage) {
+        flush_wave(a, st, staged, lane);
+        staged = 0;
+    }
+    if (changed) {
+        const int pos = staged + lane_prefix(k);
+        st.key[pos] = key;
+        st.val[pos] = val;
+    }
+    staged += cnt;
+}
+
+// Exact inverse of every queued candidate, 64 per pass; changed ones are
+// staged.  Empties the queue.
+template <bool kDecayOne>
+__device__ void drain_queue(const ExtractParams& a, const WaveStage& st, int& queued, int& staged,
+                            int lane)
+{
+    wave_sync();
+    for (int base = 0; base < queued; base += 64) {
+        const int i = base + lane;
+        bool changed = false;
+        uint32_t key = 0;
+        uint16_t bn = 0;
+        if (i < queued) {
+            const float p = st.qp[i];
+            const float ph = exact_prev<kDecayOne>(p, st.qm[i], st.qv[i], a);
+            bn = (uint16_t)bf16_bits(p);
+            changed = bf16_bits(ph) != bn;
+            key = st.qkey[i];
+        }
+        stage_changed(a, st, staged, lane, changed, key, bn);
+    }
+    queued = 0;
+    wave_sync();
 }
 
 // One wave tile of kWaveTile elements starting at element t0 of the range.
 // kFull: the tile lies inside [0, n) (no per-element bounds tests).
-template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev>
-__device__ __forceinline__ void extract_wave_tile(const ExtractParams& a, int64_t t0, int lane,
-                                                  int& staged, const WaveStage& st)
+template <bool kFull, bool kVecLoads>
+__device__ __forceinline__ void load_tile(const ExtractParams& a, int64_t t0, int lane,
+                                          f32x4* P, f32x4* M, f32x4* V)
 {
     const float* tp = a.p + t0;
     const float* tm = a.m + t0;
     const float* tv = a.v + t0;
     const int64_t rem = a.n - t0;
-    f32x4 P[kVec], M[kVec], V[kVec];
 #pragma unroll
     for (int j = 0; j < kVec; ++j) {
         const int off = (j * 64 + lane) * 4;
@@ -183,9 +240,15 @@ __device__ __forceinline__ void extract_wave_tile(const ExtractParams& a, int64_
             V[j] = load4<kVecLoads>(tv, off, rem);
         }
     }
+}
 
-    uint64_t mask[kSlots];
-    int wave_total = 0;
+template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev>
+__device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0, int lane,
+                                             int& staged, int& queued, const WaveStage& st,
+                                             uint32_t iter, const f32x4* P, const f32x4* M,
+                                             const f32x4* V)
+{
+    const int64_t rem = a.n - t0;
 #pragma unroll
     for (int j = 0; j < kVec; ++j) {
         const int off = (j * 64 + lane) * 4;
@@ -193,23 +256,30 @@ __device__ __forceinline__ void extract_wave_tile(const ExtractParams& a, int64_
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             const float p = P[j][c];
-            bool changed = false;
+            const bool in = kFull || (off + c < rem);
+            const uint32_t key = (iter << kTileBits) | (uint32_t)(off + c);
             if (kWritePrev) {
+                // theta_hat requested: the exact path for every element
                 const float ph = exact_prev<kDecayOne>(p, M[j][c], V[j][c], a);
                 prev[c] = ph;
-                changed = bf16_bits(ph) != bf16_bits(p);
+                const uint32_t bn = bf16_bits(p);
+                stage_changed(a, st, staged, lane, in && bf16_bits(ph) != bn, key, (uint16_t)bn);
             } else {
-                const bool cand = !proven_unchanged<kDecayOne>(p, M[j][c], V[j][c], a);
-                if (__ballot(cand) != 0) {
+                const bool cand = in && !proven_unchanged<kDecayOne>(p, M[j][c], V[j][c], a);
+                const uint64_t ck = __ballot(cand);
+                if (ck != 0) {
+                    const int cnt = __popcll(ck);
+                    if (queued + cnt > kQueue) drain_queue<kDecayOne>(a, st, queued, staged, lane);
                     if (cand) {
-                        const float ph = exact_prev<kDecayOne>(p, M[j][c], V[j][c], a);
-                        changed = bf16_bits(ph) != bf16_bits(p);
+                        const int pos = queued + lane_prefix(ck);
+                        st.qp[pos] = p;
+                        st.qm[pos] = M[j][c];
+                        st.qv[pos] = V[j][c];
+                        st.qkey[pos] = key;
                     }
+                    queued += cnt;
                 }
             }
-            if (!kFull) changed = changed && (off + c < rem);
-            mask[4 * j + c] = __ballot(changed);
-            wave_total += __popcll(mask[4 * j + c]);
         }
         if (kWritePrev) {
             if (kFull || (kVecLoads && off + 3 < rem)) {
@@ -221,27 +291,6 @@ __device__ __forceinline__ void extract_wave_tile(const ExtractParams& a, int64_
             }
         }
     }
-    if (wave_total == 0) return;
-
-    if (staged + wave_total > kWaveStage) {
-        flush_wave(a, st, staged, lane);
-        staged = 0;
-    }
-    int run = staged;
-#pragma unroll
-    for (int s = 0; s < kSlots; ++s) {
-        const uint64_t k = mask[s];
-        if (k != 0) {
-            if ((k >> lane) & 1ull) {
-                const int pos = run + lane_prefix(k);
-                const int e = ((s >> 2) * 64 + lane) * 4 + (s & 3);
-                st.idx[pos] = a.index_base + t0 + e;
-                st.val[pos] = (uint16_t)bf16_bits(P[s >> 2][s & 3]);
-            }
-            run += __popcll(k);
-        }
-    }
-    staged += wave_total;
 }
 
 // Wave tiles [first, last) of the range; kFull: each lies inside [0, n).
@@ -249,17 +298,34 @@ template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev>
 __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_t first,
                                                          int64_t last)
 {
-    __shared__ int64_t s_idx[kWaves][kWaveStage];
+    __shared__ uint32_t s_key[kWaves][kWaveStage];
     __shared__ uint16_t s_val[kWaves][kWaveStage];
+    __shared__ float s_qp[kWaves][kQueue];
+    __shared__ float s_qm[kWaves][kQueue];
+    __shared__ float s_qv[kWaves][kQueue];
+    __shared__ uint32_t s_qkey[kWaves][kQueue];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const WaveStage st{s_idx[wave], s_val[wave]};
-    const int64_t nwaves = (int64_t)gridDim.x * kWaves;
+    // block b owns the contiguous tile range [b per, (b+1) per); its waves
+    // take every kWaves-th tile of it, so the four waves of a block stream
+    // neighbouring tiles and each wave's output is a local, ascending run
+    const int64_t per = (last - first + gridDim.x - 1) / gridDim.x;
+    const int64_t b_first = first + (int64_t)blockIdx.x * per;
+    const int64_t b_last = (b_first + per < last) ? b_first + per : last;
+    int64_t t = b_first + wave;
     int staged = 0;
-    for (int64_t t = first + (int64_t)blockIdx.x * kWaves + wave; t < last; t += nwaves)
-        extract_wave_tile<kFull, kVecLoads, kDecayOne, kWritePrev>(a, t * kWaveTile, lane, staged,
-                                                                   st);
+    const WaveStage st{s_key[wave], s_val[wave], s_qp[wave], s_qm[wave], s_qv[wave],
+                       s_qkey[wave], t, kWaves};
+    uint32_t iter = 0;
+    int queued = 0;
+    for (; t < b_last; t += kWaves) {
+        f32x4 P[kVec], M[kVec], V[kVec];
+        load_tile<kFull, kVecLoads>(a, t * kWaveTile, lane, P, M, V);
+        process_tile<kFull, kVecLoads, kDecayOne, kWritePrev>(a, t * kWaveTile, lane, staged,
+                                                             queued, st, iter++, P, M, V);
+    }
+    if (queued > 0) drain_queue<kDecayOne>(a, st, queued, staged, lane);
     if (staged > 0) flush_wave(a, st, staged, lane);
 }
 

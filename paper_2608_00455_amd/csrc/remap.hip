@@ -7,12 +7,22 @@
 // unravels i - flat_begin over the segment's row-major shape
 // (eq. canonical_unravel), and for each operation of the segment tests
 // containment a_s <= u < a_s + e and ravels u - a_s + a_r over the
-// receiver view (eq. receiver_local_remapping).  Blocks own contiguous
-// slices of the entry list; a first pass counts each rank's outputs in LDS,
-// one atomicAdd per rank per block reserves bucket space, and a second pass
-// writes (offset, value) pairs.
+// receiver view (eq. receiver_local_remapping).
 //
-// Apply: shard[off] = val, grid-stride over each rank's bucket.
+// Work unit: a wave takes 512 consecutive entries (8 per lane) into
+// registers.  Extract emits local ascending runs, so a chunk usually lies in
+// one segment: then each operation of the segment is loaded once (into
+// scalar registers) and tested against all eight slots, one ballot per slot.
+// Chunks that span segments route slot by slot, lanes grouped by segment.
+// Each block owns a contiguous slice of the entries; pass 1 counts the
+// slice's outputs per rank, one atomicAdd per touched rank and block
+// reserves bucket space, pass 2 recomputes and writes (offset, value) at
+// the reserved positions (a few atomics per block: same-address atomics
+// serialise at the memory side, so they are kept out of the inner loops).
+//
+// Apply: shard[off] = val; each lane keeps eight independent
+// load-then-store chains in flight (the scattered 2-byte stores are
+// read-modify-write at the memory side, so parallelism is what matters).
 #include <hip/hip_runtime.h>
 
 #include "dte_internal.h"
@@ -27,39 +37,6 @@ __global__ void zero_i64_kernel(int64_t* p, int64_t n)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) p[i] = 0;
-}
-
-struct Located {
-    int32_t seg;        // -1: outside the plan
-    uint32_t u[DTE_MAX_DIMS];
-};
-
-__device__ __forceinline__ Located locate(const PlanView& pl, int64_t i)
-{
-    Located r;
-    r.seg = -1;
-    if (i < 0 || i >= pl.total) return r;
-    int32_t s = pl.lookup[i >> pl.shift];
-    while (pl.seg_begin[s + 1] <= i) ++s;                    // tiles [0, total)
-    uint32_t li = (uint32_t)(i - pl.seg_begin[s]);           // < 2^32 (validated)
-    const int nd = pl.seg_ndim[s];
-    const uint32_t* shape = pl.seg_shape + (int64_t)s * DTE_MAX_DIMS;
-#pragma unroll
-    for (int d = DTE_MAX_DIMS - 1; d >= 0; --d) {
-        if (d < nd) {
-            if (d == 0) {
-                r.u[0] = li;
-            } else {
-                const uint32_t q = li / shape[d];
-                r.u[d] = li - q * shape[d];
-                li = q;
-            }
-        } else {
-            r.u[d] = 0;
-        }
-    }
-    r.seg = s;
-    return r;
 }
 
 // Receiver offset of coordinate u under op o, or -1 when u is outside o.
@@ -77,67 +54,251 @@ __device__ __forceinline__ int64_t route(const DevOp& o, const uint32_t* u)
     return o.dst_base + j;
 }
 
+constexpr int kWaves = kBlock / 64;
+constexpr int kRemapSlots = 8;                     // entries per lane per chunk
+constexpr int kChunk = 64 * kRemapSlots;           // entries per wave per chunk
+
+__device__ __forceinline__ int lane_prefix(uint64_t mask)
+{
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+// Unravel a segment-local offset over a row-major shape of nd dimensions.
+__device__ __forceinline__ void unravel(uint32_t li, int nd, const uint32_t* shape,
+                                        uint32_t* u)
+{
+#pragma unroll
+    for (int d = DTE_MAX_DIMS - 1; d >= 0; --d) {
+        if (d < nd) {
+            if (d == 0) {
+                u[0] = li;
+            } else {
+                const uint32_t q = li / shape[d];
+                u[d] = li - q * shape[d];
+                li = q;
+            }
+        } else {
+            u[d] = 0;
+        }
+    }
+}
+
+__device__ __forceinline__ int64_t readlane64(int64_t x, int lane)
+{
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)x >> 32), lane);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Wave-uniform description of the current segment (scalar registers).
+struct SegInfo {
+    int64_t lo, hi;      // flat range [lo, hi); empty before the first lookup
+    int32_t seg, k0, k1; // operations [k0, k1)
+};
+
+// Segment holding the uniform flat offset i0 (0 <= i0 < total).
+__device__ __forceinline__ SegInfo find_segment(const PlanView& pl, int64_t i0)
+{
+    int32_t s = __builtin_amdgcn_readfirstlane(pl.lookup[i0 >> pl.shift]);
+    while (readlane64(pl.seg_begin[s + 1], 0) <= i0) ++s;
+    return SegInfo{readlane64(pl.seg_begin[s], 0), readlane64(pl.seg_begin[s + 1], 0), s,
+                   __builtin_amdgcn_readfirstlane(pl.seg_ops[s]),
+                   __builtin_amdgcn_readfirstlane(pl.seg_ops[s + 1])};
+}
+
+// One operation with every field made wave-uniform (scalar registers).
+__device__ __forceinline__ DevOp load_op(const DevOp* ops, int32_t k)
+{
+    const uint32_t* w = reinterpret_cast<const uint32_t*>(ops + k);
+    DevOp o;
+    uint32_t* d = reinterpret_cast<uint32_t*>(&o);
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(DevOp) / 4); ++i) d[i] = __builtin_amdgcn_readfirstlane(w[i]);
+    return o;
+}
+
+__device__ __forceinline__ void unravel_in(const PlanView& pl, int32_t s, uint32_t li, uint32_t* u)
+{
+    unravel(li, __builtin_amdgcn_readfirstlane(pl.seg_ndim[s]),
+            pl.seg_shape + (int64_t)s * DTE_MAX_DIMS, u);
+}
+
+// Route one slot lane by lane in groups sharing a segment (used when a
+// chunk spans several segments).  Counters: lane r of `runv` holds the
+// running count of rank first + r, lane r of `basev` the reserved bucket
+// start.  kWrite == false counts outputs; kWrite == true writes them.
+template <bool kWrite>
+__device__ __forceinline__ void route_slot(const PlanView& pl, const RankSlice& out, int lane,
+                                           int64_t i, uint16_t v, int& runv, int64_t basev,
+                                           SegInfo& cache)
+{
+    bool pending = i >= 0;
+    uint64_t pmask = __ballot(pending);
+    while (pmask != 0) {
+        const int src = __builtin_ctzll(pmask);
+        const int64_t i0 = readlane64(i, src);
+        if (!(i0 >= cache.lo && i0 < cache.hi)) cache = find_segment(pl, i0);
+        const bool mine = pending && i >= cache.lo && i < cache.hi;
+        pending = pending && !mine;
+        pmask = __ballot(pending);
+        uint32_t u[DTE_MAX_DIMS];
+        unravel_in(pl, cache.seg, (uint32_t)(i - cache.lo), u);
+        for (int32_t k = cache.k0; k < cache.k1; ++k) {
+            const DevOp o = load_op(pl.ops, k);
+            const int r = o.rank - out.first;
+            if (r < 0 || r >= out.count) continue;
+            const int64_t j = mine ? route(o, u) : -1;
+            const uint64_t b = __ballot(j >= 0);
+            if (b == 0) continue;
+            const int start = __builtin_amdgcn_readlane(runv, r);
+            if (lane == r) runv += __popcll(b);
+            if (kWrite && j >= 0) {
+                const int64_t pos = readlane64(basev, r) + start + lane_prefix(b);
+                if (pos < out.cap[r]) {
+                    out.off[r][pos] = j;
+                    out.val[r][pos] = v;
+                }
+            }
+        }
+    }
+}
+
+// Whole chunk inside one segment: each operation is loaded once and tested
+// against all slots (coordinates kept in registers).
+template <bool kWrite>
+__device__ __forceinline__ void route_chunk(const PlanView& pl, const RankSlice& out, int lane,
+                                            const SegInfo& sg, const int64_t* x, const uint16_t* y,
+                                            const uint32_t (*u)[DTE_MAX_DIMS], int& runv,
+                                            int64_t basev)
+{
+    for (int32_t k = sg.k0; k < sg.k1; ++k) {
+        const DevOp o = load_op(pl.ops, k);
+        const int r = o.rank - out.first;
+        if (r < 0 || r >= out.count) continue;
+        int run = __builtin_amdgcn_readlane(runv, r);
+        const int64_t base = kWrite ? readlane64(basev, r) : 0;
+#pragma unroll
+        for (int j = 0; j < kRemapSlots; ++j) {
+            const int64_t t = x[j] >= 0 ? route(o, u[j]) : -1;
+            const uint64_t b = __ballot(t >= 0);
+            if (kWrite && t >= 0) {
+                const int64_t pos = base + run + lane_prefix(b);
+                if (pos < out.cap[r]) {
+                    out.off[r][pos] = t;
+                    out.val[r][pos] = y[j];
+                }
+            }
+            run += __popcll(b);
+        }
+        if (lane == r) runv = run;
+    }
+}
+
+// Route the chunk of entries [c0, c1): counting pass (kWrite == false) or
+// writing pass.  Wave-uniform.
+template <bool kWrite>
+__device__ __forceinline__ void route_range(const PlanView& pl, const RankSlice& out, int lane,
+                                            const int64_t* __restrict__ idx,
+                                            const uint16_t* __restrict__ val, int64_t c0,
+                                            int64_t c1, int& runv, int64_t basev, SegInfo& cache)
+{
+    int64_t x[kRemapSlots];
+    uint16_t y[kRemapSlots];
+#pragma unroll
+    for (int j = 0; j < kRemapSlots; ++j) {     // all loads of the chunk in flight
+        int64_t e = c0 + j * 64 + lane;
+        const bool ok = e < c1;
+        e = ok ? e : c0;
+        x[j] = idx[e];
+        y[j] = kWrite ? val[e] : (uint16_t)0;
+        x[j] = (ok && x[j] >= 0 && x[j] < pl.total) ? x[j] : -1;   // outside: ignored
+    }
+    // does one segment hold the whole chunk?
+    uint64_t any = 0;
+    int64_t i0 = 0;
+#pragma unroll
+    for (int j = kRemapSlots - 1; j >= 0; --j) {
+        const uint64_t b = __ballot(x[j] >= 0);
+        if (b) {
+            any = b;
+            i0 = readlane64(x[j], __builtin_ctzll(b));
+        }
+    }
+    if (any == 0) return;
+    if (!(i0 >= cache.lo && i0 < cache.hi)) cache = find_segment(pl, i0);
+    bool inside = true;
+#pragma unroll
+    for (int j = 0; j < kRemapSlots; ++j)
+        inside = inside && (x[j] < 0 || (x[j] >= cache.lo && x[j] < cache.hi));
+    if (__ballot(!inside) == 0) {
+        uint32_t u[kRemapSlots][DTE_MAX_DIMS];
+#pragma unroll
+        for (int j = 0; j < kRemapSlots; ++j)
+            unravel_in(pl, cache.seg, (uint32_t)(x[j] - cache.lo), u[j]);
+        route_chunk<kWrite>(pl, out, lane, cache, x, y, u, runv, basev);
+    } else {
+#pragma unroll 1
+        for (int j = 0; j < kRemapSlots; ++j)
+            route_slot<kWrite>(pl, out, lane, x[j], y[j], runv, basev, cache);
+    }
+}
+
+// Block b owns entries [total b / G, total (b+1) / G); its waves take every
+// fourth chunk.  Pass 1 counts per rank, the block reserves bucket space
+// with one atomicAdd per rank, pass 2 writes: wave w of the block writes
+// after the outputs of waves 0..w-1, each wave in its own chunk order.
 __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_t* __restrict__ idx,
                                                        const uint16_t* __restrict__ val,
                                                        const int64_t* __restrict__ count,
                                                        int64_t in_capacity, RankSlice out,
                                                        int64_t* __restrict__ rank_count)
 {
-    __shared__ int s_cnt[kRanksPerLaunch];
+    __shared__ int s_cnt[kWaves][kRanksPerLaunch];
     __shared__ int64_t s_base[kRanksPerLaunch];
 
     int64_t total = *count;
     if (total > in_capacity) total = in_capacity;
     if (total < 0) total = 0;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
     const int64_t lo = total * blockIdx.x / gridDim.x;
     const int64_t hi = total * (blockIdx.x + 1) / gridDim.x;
-    if (threadIdx.x < kRanksPerLaunch) s_cnt[threadIdx.x] = 0;
-    __syncthreads();
+    SegInfo cache{0, 0, 0, 0, 0};
 
-    // pass 1: count this block's outputs per rank
-    for (int64_t e = lo + threadIdx.x; e < hi; e += kBlock) {
-        const Located L = locate(pl, idx[e]);
-        if (L.seg < 0) continue;
-        for (int32_t k = pl.seg_ops[L.seg]; k < pl.seg_ops[L.seg + 1]; ++k) {
-            const DevOp& o = pl.ops[k];
-            const int r = o.rank - out.first;
-            if (r < 0 || r >= out.count) continue;
-            if (route(o, L.u) >= 0) atomicAdd(&s_cnt[r], 1);
-        }
+    int runv = 0;                                       // lane r: outputs for rank first + r
+    for (int64_t c0 = lo + (int64_t)wave * kChunk; c0 < hi; c0 += (int64_t)kWaves * kChunk)
+        route_range<false>(pl, out, lane, idx, val, c0, c0 + kChunk < hi ? c0 + kChunk : hi, runv,
+                           0, cache);
+    if (lane < kRanksPerLaunch) s_cnt[wave][lane] = lane < out.count ? runv : 0;
+    __syncthreads();
+    if (wave == 0 && lane < out.count) {
+        int64_t n = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) n += s_cnt[w][lane];
+        s_base[lane] = n > 0 ? (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(
+                                                      &rank_count[out.first + lane]),
+                                                  (unsigned long long)n)
+                             : 0;
     }
     __syncthreads();
-    if (threadIdx.x < out.count && s_cnt[threadIdx.x] > 0)
-        s_base[threadIdx.x] = (int64_t)atomicAdd(
-            reinterpret_cast<unsigned long long*>(&rank_count[out.first + threadIdx.x]),
-            (unsigned long long)s_cnt[threadIdx.x]);
-    __syncthreads();
-    if (threadIdx.x < kRanksPerLaunch) s_cnt[threadIdx.x] = 0;
-    __syncthreads();
-
-    // pass 2: write (receiver offset, value)
-    for (int64_t e = lo + threadIdx.x; e < hi; e += kBlock) {
-        const Located L = locate(pl, idx[e]);
-        if (L.seg < 0) continue;
-        const uint16_t v = val[e];
-        for (int32_t k = pl.seg_ops[L.seg]; k < pl.seg_ops[L.seg + 1]; ++k) {
-            const DevOp& o = pl.ops[k];
-            const int r = o.rank - out.first;
-            if (r < 0 || r >= out.count) continue;
-            const int64_t j = route(o, L.u);
-            if (j < 0) continue;
-            const int64_t pos = s_base[r] + atomicAdd(&s_cnt[r], 1);
-            if (pos < out.cap[r]) {
-                out.off[r][pos] = j;
-                out.val[r][pos] = v;
-            }
-        }
+    int64_t basev = 0;
+    if (lane < out.count) {
+        basev = s_base[lane];
+        for (int w = 0; w < wave; ++w) basev += s_cnt[w][lane];
     }
+    runv = 0;
+    for (int64_t c0 = lo + (int64_t)wave * kChunk; c0 < hi; c0 += (int64_t)kWaves * kChunk)
+        route_range<true>(pl, out, lane, idx, val, c0, c0 + kChunk < hi ? c0 + kChunk : hi, runv,
+                          basev, cache);
 }
+
+constexpr int kApplyUnroll = 8;
 
 __global__ __launch_bounds__(kBlock) void apply_kernel(ApplySlice s,
                                                       const int64_t* __restrict__ rank_count)
 {
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    const int64_t nthreads = (int64_t)gridDim.x * kBlock;
     const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     for (int r = 0; r < s.count; ++r) {
         int64_t n = rank_count[s.first + r];
@@ -146,9 +307,18 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(ApplySlice s,
         const uint16_t* val = s.val[r];
         uint16_t* shard = s.shard[r];
         const int64_t numel = s.numel[r];
-        for (int64_t e = t; e < n; e += stride) {
-            const int64_t j = off[e];
-            if (j >= 0 && j < numel) shard[j] = val[e];
+        for (int64_t e0 = t; e0 < n; e0 += nthreads * kApplyUnroll) {
+            int64_t j[kApplyUnroll];
+            uint16_t v[kApplyUnroll];
+#pragma unroll
+            for (int k = 0; k < kApplyUnroll; ++k) {
+                const int64_t e = e0 + k * nthreads;
+                j[k] = e < n ? off[e] : -1;
+                v[k] = e < n ? val[e] : (uint16_t)0;
+            }
+#pragma unroll
+            for (int k = 0; k < kApplyUnroll; ++k)
+                if (j[k] >= 0 && j[k] < numel) shard[j[k]] = v[k];
         }
     }
 }
@@ -168,9 +338,7 @@ hipError_t launch_remap(const PlanView& plan, const int64_t* idx, const uint16_t
                         int64_t* rank_count, int cus, hipStream_t stream)
 {
     if (in_capacity <= 0) return hipSuccess;
-    const int64_t want = (int64_t)cus * kBlocksPerCU;
-    const int64_t need = (in_capacity + kBlock - 1) / kBlock;
-    const dim3 grid((unsigned)(need < want ? need : want));
+    const dim3 grid((unsigned)cus * kBlocksPerCU);     // persistent: the count is on the device
     hipLaunchKernelGGL(remap_kernel, grid, dim3(kBlock), 0, stream, plan, idx, val, count,
                        in_capacity, out, rank_count);
     return hipGetLastError();
@@ -179,7 +347,7 @@ hipError_t launch_remap(const PlanView& plan, const int64_t* idx, const uint16_t
 hipError_t launch_apply(const ApplySlice& s, const int64_t* rank_count, int cus,
                         hipStream_t stream)
 {
-    const dim3 grid((unsigned)cus * kBlocksPerCU);
+    const dim3 grid((unsigned)cus * 8);
     hipLaunchKernelGGL(apply_kernel, grid, dim3(kBlock), 0, stream, s, rank_count);
     return hipGetLastError();
 }

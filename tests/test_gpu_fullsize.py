@@ -42,6 +42,20 @@ def sentinel_shards(spec):
     return [torch.full((n,), SENTINEL, dtype=torch.int16, device="cuda") for n in spec.rank_numel]
 
 
+def golden_diag(name):
+    import json
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "diagnostics.json")
+    return json.load(open(path))["workloads"][name]
+
+
+def check_oracle_diag(wl, res):
+    g = golden_diag(wl.name)
+    d = res.diag
+    assert (d.n, d.changed, d.bf16_recon_mismatch, d.fp32_recon_mismatch) == \
+        (g["elements"], g["changed"], g["bf16_recon_mismatch"], g["fp32_recon_mismatch"])
+
+
 def check_delta(pipe, res):
     idx, val, total = pipe.delta()
     assert total == res.idx.size, (total, res.idx.size)
@@ -104,6 +118,7 @@ def qwen3_8b():
     say("fullsize: oracle over %s (%d elements)" % (wl.name, wl.numel))
     res = orun.extract(wl)
     say("fullsize: oracle done, %d changed, %s" % (res.idx.size, res.diag))
+    check_oracle_diag(wl, res)
     p, m, v = generate_state(wl)
     yield wl, res, p, m, v
     del p, m, v
@@ -145,6 +160,7 @@ def test_qwen3_30b_a3b_share_full():
     say("fullsize: oracle over %s (%d elements)" % (wl.name, wl.numel))
     res = orun.extract(wl)
     say("fullsize: oracle done, %d changed, %s" % (res.idx.size, res.diag))
+    check_oracle_diag(wl, res)
     # untouched experts (zero moments) never change
     begins = wl.flat_begins()
     for k, t in enumerate(wl.tensors):
@@ -173,6 +189,7 @@ def test_qwen3_8b_layers_lr_sweep_full(lr):
     wl = W.qwen3_8b_layers_sweep(lr)
     say("fullsize: sweep lr %g" % lr)
     res = orun.extract(wl)
+    check_oracle_diag(wl, res)
     p, m, v = generate_state(wl)
     spec = layouts.build_spec(wl)
     pl = oplan.build_plan(wl)

@@ -78,3 +78,17 @@ def test_lr_zero_gives_empty_delta():
     wl = W.scaled_dense(layers=1, tp=2)
     res = orun.extract(wl, hp=W.StepHP(lr=0.0), threads=1)
     assert res.idx.size == 0 and res.diag.fp32_recon_mismatch == 0
+
+
+def test_tiny_block_diagnostics_match_golden():
+    """Regression pin of the oracle's counts (tests/golden/diagnostics.json,
+    written by python -m oracle.diagnostics)."""
+    import json
+    import os
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                       "diagnostics.json")))["workloads"]["tiny_block_tp2"]
+    d = orun.extract(W.tiny_block()).diag
+    assert (d.n, d.changed, d.bf16_recon_mismatch, d.fp32_recon_mismatch, d.true_changed,
+            d.apply_vs_prev_diff) == (gold["elements"], gold["changed"],
+                                      gold["bf16_recon_mismatch"], gold["fp32_recon_mismatch"],
+                                      gold["true_changed"], gold["apply_vs_prev_diff"])

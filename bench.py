@@ -12,8 +12,10 @@ elements/s, the roofline of the dominant kernel (extract, HBM-bound) and
 the CPU oracle's throughput on a bounded sample of the same workload.
 
 Other workloads (--workload): tiny_block_tp2, qwen3_30b_a3b_12l_ep8,
-qwen3_8b_4l_tp4 (with --lr), qwen3_8b_tp8_apply (apply-only timing of the
-Qwen3-8B delta into eight TP=8 shards).
+qwen3_8b_4l_tp4 (with --lr), qwen3_8b_4l_mcore (four Qwen3-8B layers held as
+the Megatron-Core shard of trainer TP rank 1 of 2, receiver TP=4),
+qwen3_8b_tp8_apply (apply-only timing of the Qwen3-8B delta into eight TP=8
+shards).
 """
 from __future__ import annotations
 
@@ -46,6 +48,8 @@ def workload(name, lr):
         return W.qwen3_30b_a3b_share(synth.word)
     if name == "qwen3_8b_4l_tp4":
         return W.qwen3_8b_layers_sweep(lr if lr is not None else 1e-6)
+    if name == "qwen3_8b_4l_mcore":
+        return W.qwen3_8b_layers_mcore(trainer_rank=1, lr=lr if lr is not None else 1e-6)
     raise SystemExit("unknown workload %r" % name)
 
 
@@ -166,12 +170,12 @@ def main():
         return copy_calibration(args.copy_calibration)
     wl = workload(args.workload, args.lr)
     hp = wl.hp if args.lr is None else type(wl.hp)(lr=args.lr)
-    n = wl.numel
+    spec = layouts.build_spec(wl)
+    n = spec.total                           # elements of the trainer shard
     log("bench: workload %s, %d elements, lr %g" % (wl.name, n, hp.lr))
     t = time.perf_counter()
     p, m, v = generate_state(wl, hp)
     log("bench: state generated in %.1f s" % (time.perf_counter() - t))
-    spec = layouts.build_spec(wl)
     frac = args.capacity_fraction
     if frac is None:
         frac = 0.25 if args.workload == "qwen3_8b_4l_tp4" else 0.02

@@ -5,8 +5,17 @@ Observation 3: the layouts fix it before synchronisation).
 Host-side metadata only: the result is handed to dte_plan_create, which
 validates it (coverage, bounds, single writer per receiver element).
 
-Sender side: the flat trainer shard holds the canonical (Hugging Face)
-tensors back to back in parameter order; each is one dte_segment.
+Sender side: the flat trainer shard is a sequence of segments (one
+dte_segment each).  With the canonical layout they are the Hugging Face
+tensors in parameter order.  With the Megatron-Core layout they are one
+trainer tensor-parallel rank's optimizer-native tensors, and the converter
+of sec. 3.2.1 (appendix B) is folded into the plan: each segment is a set of
+pieces, each piece a box of the segment that is a box of one canonical
+tensor (fused linear_qkv: per key/value group j the g query heads, then K_j,
+then V_j, eq. mcore_fused_qkv, rank r holding rows R_r, eq. mcore_tp_shard;
+linear_fc1: [gate_r; up_r]; linear_proj / linear_fc2: input columns of the
+rank; layernorms whole), and every plan operation is the intersection of a
+sender piece with a receiver piece of the same canonical tensor.
 Receiver side, per rank, a flat BF16 buffer of consecutive tensors:
   dense, tensor parallel degree P (rank r):
     embed_tokens / lm_head  rows [r V/P, (r+1) V/P)
@@ -31,10 +40,29 @@ from .binding import DTE_MAX_DIMS, dte_op, dte_segment
 
 @dataclass
 class Piece:
-    segment: int
+    """Receiver piece: box [src_lo, src_lo + extent) of canonical tensor
+    `tensor` placed at dst_lo of a receiver view."""
+    tensor: int
     src_lo: Tuple[int, ...]
     extent: Tuple[int, ...]
     dst_lo: Tuple[int, ...]
+
+
+@dataclass
+class SPiece:
+    """Sender piece: box [local_lo, local_lo + extent) of a sender segment
+    holding box [canon_lo, canon_lo + extent) of canonical tensor `tensor`."""
+    local_lo: Tuple[int, ...]
+    extent: Tuple[int, ...]
+    tensor: int
+    canon_lo: Tuple[int, ...]
+
+
+@dataclass
+class SenderSeg:
+    name: str
+    shape: Tuple[int, ...]
+    pieces: List[SPiece]
 
 
 @dataclass
@@ -46,21 +74,14 @@ class View:
 
 @dataclass
 class PlanSpec:
-    segments: List[Tuple[int, Tuple[int, ...]]]      # (flat_begin, shape)
+    segments: List[Tuple[int, Tuple[int, ...]]]      # (flat_begin, shape) of sender segments
     views: List[List[Tuple[int, View]]]               # per rank: (flat base, view)
     rank_numel: List[int]
+    senders: List[SenderSeg] = field(default_factory=list)
 
     @property
     def nranks(self) -> int:
         return len(self.rank_numel)
-
-    @property
-    def total(self) -> int:
-        b, s = self.segments[-1]
-        n = 1
-        for x in s:
-            n *= x
-        return b + n
 
     def c_segments(self) -> List[dte_segment]:
         out = []
@@ -74,22 +95,43 @@ class PlanSpec:
         return out
 
     def c_ops(self) -> List[dte_op]:
+        by_tensor: Dict[int, List[Tuple[int, SPiece]]] = {}
+        for si, seg in enumerate(self.senders):
+            for sp in seg.pieces:
+                by_tensor.setdefault(sp.tensor, []).append((si, sp))
         ops = []
         for rank, views in enumerate(self.views):
             for base, vw in views:
+                nd = len(vw.shape)
                 for pc in vw.pieces:
-                    o = dte_op()
-                    o.segment = pc.segment
-                    o.rank = rank
-                    o.dst_base = base
-                    nd = len(vw.shape)
-                    for d in range(DTE_MAX_DIMS):
-                        o.src_origin[d] = pc.src_lo[d] if d < nd else 0
-                        o.extent[d] = pc.extent[d] if d < nd else 1
-                        o.dst_origin[d] = pc.dst_lo[d] if d < nd else 0
-                        o.dst_shape[d] = vw.shape[d] if d < nd else 1
-                    ops.append(o)
+                    for si, sp in by_tensor.get(pc.tensor, []):
+                        lo = [max(pc.src_lo[d], sp.canon_lo[d]) for d in range(nd)]
+                        hi = [min(pc.src_lo[d] + pc.extent[d], sp.canon_lo[d] + sp.extent[d])
+                              for d in range(nd)]
+                        if any(lo[d] >= hi[d] for d in range(nd)):
+                            continue
+                        o = dte_op()
+                        o.segment = si
+                        o.rank = rank
+                        o.dst_base = base
+                        for d in range(DTE_MAX_DIMS):
+                            used = d < nd
+                            o.src_origin[d] = sp.local_lo[d] + lo[d] - sp.canon_lo[d] if used else 0
+                            o.extent[d] = hi[d] - lo[d] if used else 1
+                            o.dst_origin[d] = pc.dst_lo[d] + lo[d] - pc.src_lo[d] if used else 0
+                            o.dst_shape[d] = vw.shape[d] if used else 1
+                        ops.append(o)
         return ops
+
+    @property
+    def total(self) -> int:
+        if not self.segments:
+            return 0
+        b, shp = self.segments[-1]
+        n = 1
+        for x in shp:
+            n *= x
+        return b + n
 
 
 def _part(total: int, parts: int, i: int) -> Tuple[int, int]:
@@ -196,12 +238,90 @@ def _moe_rank(ix, r, R, A, E):
     return views
 
 
+def _whole_piece(shape, k):
+    return SPiece((0,) * len(shape), tuple(shape), k, (0,) * len(shape))
+
+
+def sender_segments(wl) -> List[SenderSeg]:
+    """The trainer shard's segments and their canonical pieces."""
+    ix = _Index(wl)
+    sd = wl.sender
+    if sd.kind == "canonical":
+        return [SenderSeg(t.name, tuple(t.shape), [_whole_piece(t.shape, k)])
+                for k, t in enumerate(wl.tensors)]
+    if sd.kind != "mcore":
+        raise ValueError("unknown sender layout %r" % sd.kind)
+    if wl.receiver.kind != "tp":
+        raise ValueError("the Megatron-Core sender layout is built for dense models")
+    P, r = sd.tp, sd.rank
+    d = wl.dims
+    g, dh = d.heads_q // d.heads_kv, d.head_dim
+    segs: List[SenderSeg] = []
+
+    def whole(k, name):
+        segs.append(SenderSeg(name, ix.shape(k), [_whole_piece(ix.shape(k), k)]))
+
+    def row_slice(k, name):
+        rows, cols = ix.shape(k)
+        lo, n = _part(rows, P, r)
+        segs.append(SenderSeg(name, (n, cols), [SPiece((0, 0), (n, cols), k, (lo, 0))]))
+
+    def col_slice(k, name):
+        rows, cols = ix.shape(k)
+        lo, n = _part(cols, P, r)
+        segs.append(SenderSeg(name, (rows, n), [SPiece((0, 0), (rows, n), k, (0, lo))]))
+
+    emb = ix.seg(None, "embed")
+    if emb is not None:
+        row_slice(emb, "embedding.word_embeddings.weight")
+    for L in ix.layers:
+        pre = "decoder.layers.%d." % L
+        whole(ix.seg(L, "in_norm"), pre + "self_attention.linear_qkv.layer_norm_weight")
+        q, k, v = ix.seg(L, "q"), ix.seg(L, "k"), ix.seg(L, "v")
+        h = ix.shape(q)[1]
+        j0, nj = _part(d.heads_kv, P, r)          # key/value groups of this rank
+        per_group = (g + 2) * dh
+        pieces = []
+        for jj in range(nj):
+            j = j0 + jj
+            base = jj * per_group
+            pieces.append(SPiece((base, 0), (g * dh, h), q, (j * g * dh, 0)))
+            pieces.append(SPiece((base + g * dh, 0), (dh, h), k, (j * dh, 0)))
+            pieces.append(SPiece((base + (g + 1) * dh, 0), (dh, h), v, (j * dh, 0)))
+        segs.append(SenderSeg(pre + "self_attention.linear_qkv.weight", (nj * per_group, h),
+                              pieces))
+        for role, nm in (("q_norm", "q_layernorm"), ("k_norm", "k_layernorm")):
+            kk = ix.seg(L, role)
+            if kk is not None:
+                whole(kk, pre + "self_attention." + nm + ".weight")
+        col_slice(ix.seg(L, "o"), pre + "self_attention.linear_proj.weight")
+        whole(ix.seg(L, "post_norm"), pre + "mlp.linear_fc1.layer_norm_weight")
+        gt, up = ix.seg(L, "gate"), ix.seg(L, "up")
+        rows, cols = ix.shape(gt)
+        lo, n = _part(rows, P, r)
+        segs.append(SenderSeg(pre + "mlp.linear_fc1.weight", (2 * n, cols),
+                              [SPiece((0, 0), (n, cols), gt, (lo, 0)),
+                               SPiece((n, 0), (n, cols), up, (lo, 0))]))
+        col_slice(ix.seg(L, "down"), pre + "mlp.linear_fc2.weight")
+    fn = ix.seg(None, "final_norm")
+    if fn is not None:
+        whole(fn, "decoder.final_layernorm.weight")
+    head = ix.seg(None, "lm_head")
+    if head is not None:
+        row_slice(head, "output_layer.weight")
+    return segs
+
+
 def build_spec(wl) -> PlanSpec:
     ix = _Index(wl)
+    senders = sender_segments(wl)
     segments, pos = [], 0
-    for t in wl.tensors:
-        segments.append((pos, tuple(t.shape)))
-        pos += t.numel
+    for sg in senders:
+        segments.append((pos, tuple(sg.shape)))
+        n = 1
+        for x in sg.shape:
+            n *= x
+        pos += n
     rc = wl.receiver
     per_rank = []
     for r in range(rc.nranks):
@@ -225,4 +345,4 @@ def build_spec(wl) -> PlanSpec:
             base += n
         placed.append(lst)
         numel.append(base)
-    return PlanSpec(segments, placed, numel)
+    return PlanSpec(segments, placed, numel, senders)

@@ -129,34 +129,57 @@ class _null:
 
 
 def generate_state(wl, hp=None, device="cuda"):
-    """Post-step state (p, m, v) of workload `wl` on the device.
+    """Post-step state (p, m, v) of workload `wl` on the device, laid out as
+    the trainer shard (the sender segments of `layouts.sender_segments`).
 
-    Seeded pre-step draws per tensor (synth), then one dte_adamw_forward
-    over the whole flat shard.  Untouched tensors get zero moments and
-    gradient.  Returns three flat float32 tensors of wl.numel elements.
+    Every element is drawn (synth) at its canonical coordinates, so the
+    canonical and Megatron-Core layouts hold the same model state; then one
+    dte_adamw_forward over the whole flat shard.  Untouched tensors get zero
+    moments and gradient.  Returns three flat float32 tensors.
     """
     import synth
     from synth.workloads import KIND_GRAD, KIND_M_PREV, KIND_P_PREV, KIND_V_PREV
 
+    from .layouts import sender_segments
+
     hp = hp or wl.hp
-    n = wl.numel
+    segs = sender_segments(wl)
+    n = 0
+    for sg in segs:
+        k = 1
+        for x in sg.shape:
+            k *= x
+        n += k
     dev = torch.device(device)
     p = torch.empty(n, dtype=torch.float32, device=dev)
     m = torch.empty(n, dtype=torch.float32, device=dev)
     v = torch.empty(n, dtype=torch.float32, device=dev)
     g = torch.empty(n, dtype=torch.float32, device=dev)
     s = torch.cuda.current_stream().cuda_stream
-    for k, (t, begin) in enumerate(zip(wl.tensors, wl.flat_begins())):
-        sl = slice(begin, begin + t.numel)
-        synth.fill_gpu(p[sl].data_ptr(), t.numel, wl.seed, k, KIND_P_PREV, 0, s)
-        if t.touched:
-            synth.fill_gpu(m[sl].data_ptr(), t.numel, wl.seed, k, KIND_M_PREV, 0, s)
-            synth.fill_gpu(v[sl].data_ptr(), t.numel, wl.seed, k, KIND_V_PREV, 0, s)
-            synth.fill_gpu(g[sl].data_ptr(), t.numel, wl.seed, k, KIND_GRAD, 0, s)
-        else:
-            m[sl].zero_()
-            v[sl].zero_()
-            g[sl].zero_()
+    kinds = ((p, KIND_P_PREV), (m, KIND_M_PREV), (v, KIND_V_PREV), (g, KIND_GRAD))
+    begin = 0
+    for sg in segs:
+        numel = 1
+        for x in sg.shape:
+            numel *= x
+        for sp in sg.pieces:
+            t = wl.tensors[sp.tensor]
+            whole = tuple(sp.extent) == tuple(t.shape)
+            assert not whole or not any(sp.local_lo)
+            for buf, kind in kinds:
+                if kind != KIND_P_PREV and not t.touched:
+                    buf[begin:begin + numel].zero_()
+                    continue
+                if whole:
+                    synth.fill_gpu(buf[begin:].data_ptr(), t.numel, wl.seed, sp.tensor, kind, 0, s)
+                else:
+                    # 2-D piece: extent rows x cols at local_lo of the segment
+                    cols = sg.shape[1]
+                    first = begin + sp.local_lo[0] * cols + sp.local_lo[1]
+                    synth.fill_gpu_2d(buf[first:].data_ptr(), sp.extent[0], sp.extent[1], cols,
+                                      wl.seed, sp.tensor, kind, sp.canon_lo[0], sp.canon_lo[1],
+                                      t.shape[1], s)
+        begin += numel
     B.dte_adamw_forward(p.data_ptr(), m.data_ptr(), v.data_ptr(), g.data_ptr(), n, hp, s)
     torch.cuda.current_stream().synchronize()
     del g

@@ -41,6 +41,10 @@ def _load_cpu():
         lib.synth_fill_cpu.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
                                        ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64,
                                        ctypes.c_double, ctypes.c_int]
+        lib.synth_fill_2d_cpu.restype = None
+        lib.synth_fill_2d_cpu.argtypes = [ctypes.c_void_p] + [ctypes.c_int64] * 3 + [
+            ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32] + [ctypes.c_int64] * 3 + [
+            ctypes.c_double, ctypes.c_int]
         lib.synth_philox_block.restype = None
         lib.synth_philox_block.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         _cpu = lib
@@ -53,6 +57,10 @@ def _load_hip():
         if not os.path.exists(HIP_LIB):
             raise RuntimeError("synth: %s is not built (run __graft_entry__.build())" % HIP_LIB)
         lib = ctypes.CDLL(HIP_LIB)
+        lib.synth_fill_2d_hip.restype = ctypes.c_int
+        lib.synth_fill_2d_hip.argtypes = [ctypes.c_void_p] + [ctypes.c_int64] * 3 + [
+            ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32] + [ctypes.c_int64] * 3 + [
+            ctypes.c_double, ctypes.c_int, ctypes.c_void_p]
         lib.synth_fill_hip.restype = ctypes.c_int
         lib.synth_fill_hip.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
                                        ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64,
@@ -125,3 +133,27 @@ def fill_gpu(ptr: int, n: int, seed: int, tensor: int, kind: int, index_base: in
                             _load_cpu().synth_scale(SIGMA[kind]), ABSVAL[kind], stream)
     if rc != 0:
         raise RuntimeError("synth_fill_hip failed with hipError %d" % rc)
+
+
+def fill_cpu_2d(out: np.ndarray, seed: int, tensor: int, kind: int, row0: int, col0: int,
+                canon_ncols: int) -> np.ndarray:
+    """Fill a 2-D float32 host array (rows may be strided) with the draws of
+    the canonical block starting at (row0, col0) of a tensor with
+    canon_ncols columns."""
+    assert out.dtype == np.float32 and out.ndim == 2 and out.strides[1] == 4
+    lib = _load_cpu()
+    lib.synth_fill_2d_cpu(out.ctypes.data, out.shape[0], out.shape[1], out.strides[0] // 4, seed,
+                          tensor, kind, row0, col0, canon_ncols, lib.synth_scale(SIGMA[kind]),
+                          ABSVAL[kind])
+    return out
+
+
+def fill_gpu_2d(ptr: int, nrows: int, ncols: int, row_stride: int, seed: int, tensor: int,
+                kind: int, row0: int, col0: int, canon_ncols: int, stream: int = 0) -> None:
+    """Device version of fill_cpu_2d (row_stride in elements)."""
+    lib = _load_hip()
+    rc = lib.synth_fill_2d_hip(ptr, nrows, ncols, row_stride, seed, tensor, kind, row0, col0,
+                               canon_ncols, _load_cpu().synth_scale(SIGMA[kind]), ABSVAL[kind],
+                               stream)
+    if rc != 0:
+        raise RuntimeError("synth_fill_2d_hip failed with hipError %d" % rc)

@@ -35,3 +35,16 @@ void synth_fill_cpu(float* out, int64_t n, uint64_t seed, uint32_t tensor, uint3
     for (int64_t i = 0; i < n; ++i)
         out[i] = synth_draw(seed, tensor, kind, index_base + (uint64_t)i, scale, absval);
 }
+
+/* 2-D block: out[r * row_stride + c] = draw at canonical flat index
+ * (row0 + r) * canon_ncols + col0 + c, for r < nrows, c < ncols. */
+void synth_fill_2d_cpu(float* out, int64_t nrows, int64_t ncols, int64_t row_stride,
+                       uint64_t seed, uint32_t tensor, uint32_t kind, int64_t row0, int64_t col0,
+                       int64_t canon_ncols, double scale, int absval)
+{
+    for (int64_t r = 0; r < nrows; ++r) {
+        const uint64_t base = (uint64_t)((row0 + r) * canon_ncols + col0);
+        for (int64_t c = 0; c < ncols; ++c)
+            out[r * row_stride + c] = synth_draw(seed, tensor, kind, base + (uint64_t)c, scale, absval);
+    }
+}

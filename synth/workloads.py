@@ -85,6 +85,25 @@ class Receiver:
 
 
 @dataclass(frozen=True)
+class Sender:
+    """Trainer-side layout of the flat shard.
+
+    kind 'canonical': the canonical tensors back to back in parameter order.
+    kind 'mcore': the optimizer-native Megatron-Core tensors of tensor
+    parallel rank `rank` of `tp` (per layer: input layernorm, fused
+    linear_qkv rows of the rank, q/k layernorms, linear_proj input columns
+    of the rank, pre-MLP layernorm, fused linear_fc1 [gate; up] rows of the
+    rank, linear_fc2 input columns of the rank; before the layers the
+    embedding's vocabulary rows of the rank, after them the final layernorm
+    and the output layer's vocabulary rows of the rank).  Values are drawn per
+    canonical element, so the same model state is seen in either layout.
+    """
+    kind: str = "canonical"
+    tp: int = 1
+    rank: int = 0
+
+
+@dataclass(frozen=True)
 class ModelDims:
     hidden: int
     heads_q: int
@@ -107,6 +126,7 @@ class Workload:
     hp: StepHP
     receiver: Receiver
     sweep_lr: Tuple[float, ...] = field(default_factory=tuple)
+    sender: Sender = field(default_factory=Sender)
 
     @property
     def numel(self) -> int:
@@ -284,3 +304,50 @@ def scaled_moe(word_fn, layers: int = 2, ranks: int = 4, attn_tp: int = 2, exper
                     tuple(ts), StepHP(lr=lr),
                     Receiver("moe_ep", ranks=ranks, attn_tp=attn_tp,
                              experts_per_rank=experts // ranks))
+
+
+def qwen3_8b_layers_mcore(layers: int = 4, trainer_tp: int = 2, trainer_rank: int = 0,
+                          receiver_tp: int = 4, lr: float = 1e-6) -> Workload:
+    """`layers` Qwen3-8B layers held as one trainer TP rank's Megatron-Core
+    shard; receiver TP=receiver_tp (canonical tensors as qwen3_8b_layers_sweep)."""
+    return Workload("qwen3_8b_%dl_mcore_tp%dr%d_to_tp%d" % (layers, trainer_tp, trainer_rank,
+                                                           receiver_tp),
+                    "%d Qwen3-8B layers, Megatron-Core shard of trainer TP rank %d/%d, "
+                    "receiver TP=%d" % (layers, trainer_rank, trainer_tp, receiver_tp),
+                    SEED_BASE + 6, QWEN3_8B, _qwen3_8b_tensors(layers, False), StepHP(lr=lr),
+                    Receiver("tp", tp=receiver_tp), sender=Sender("mcore", trainer_tp,
+                                                                  trainer_rank))
+
+
+def scaled_mcore(layers: int = 2, trainer_tp: int = 2, trainer_rank: int = 0,
+                 receiver_tp: int = 2, seed: int = SEED_BASE + 17, hidden=64, heads_q=8,
+                 heads_kv=4, head_dim=16, intermediate=96, vocab=0, lr=1e-5) -> Workload:
+    """Small dense model held as a Megatron-Core trainer shard (with
+    embedding, final norm and output layer when vocab > 0)."""
+    d = ModelDims(hidden=hidden, heads_q=heads_q, heads_kv=heads_kv, head_dim=head_dim,
+                  intermediate=intermediate, vocab=vocab)
+    ts = []
+    if vocab:
+        ts.append(Tensor("model.embed_tokens.weight", (vocab, hidden), "embed"))
+    for layer in range(layers):
+        ts += _dense_layer(d, layer, True)
+    if vocab:
+        ts.append(Tensor("model.norm.weight", (hidden,), "final_norm"))
+        ts.append(Tensor("lm_head.weight", (vocab, hidden), "lm_head"))
+    return Workload("dense_small_%dl_mcore_tp%dr%d_to_tp%d" % (layers, trainer_tp, trainer_rank,
+                                                              receiver_tp),
+                    "small dense model, Megatron-Core shard", seed, d, tuple(ts), StepHP(lr=lr),
+                    Receiver("tp", tp=receiver_tp), sender=Sender("mcore", trainer_tp,
+                                                                  trainer_rank))
+
+
+def with_sender_rank(wl: Workload, rank: int) -> Workload:
+    """The same workload seen from another trainer TP rank."""
+    return Workload(wl.name, wl.description, wl.seed, wl.dims, wl.tensors, wl.hp, wl.receiver,
+                    wl.sweep_lr, Sender(wl.sender.kind, wl.sender.tp, rank))
+
+
+def canonical_twin(wl: Workload) -> Workload:
+    """The same model state with the canonical sender layout."""
+    return Workload(wl.name + "_canonical", wl.description + " (canonical layout)", wl.seed,
+                    wl.dims, wl.tensors, wl.hp, wl.receiver, wl.sweep_lr, Sender())

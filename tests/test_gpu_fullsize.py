@@ -201,3 +201,35 @@ def test_qwen3_8b_layers_lr_sweep_full(lr):
     pipe.close()
     del pipe, p, m, v
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("rank", [1])
+def test_qwen3_8b_layers_mcore_full(rank):
+    """Four Qwen3-8B layers held as trainer TP rank `rank` of 2 in the
+    Megatron-Core layout, sent to four TP=4 receivers.  The oracle detects
+    in the paper's order (MCore inversion, conversion, canonical BF16
+    comparison) and routes through the canonical plan."""
+    from oracle import mcore
+    wl = W.qwen3_8b_layers_mcore(trainer_rank=rank)
+    say("fullsize: mcore oracle over %s" % wl.name)
+    want = mcore.extract(wl)
+    ci = mcore.canonical_index(wl)
+    say("fullsize: mcore oracle done, %d changed of %d" % (want.idx.size, ci.size))
+    twin = W.canonical_twin(wl)
+    cplan = oplan.build_plan(twin)
+    p, m, v = generate_state(wl)
+    spec = layouts.build_spec(wl)
+    assert spec.total == ci.size == p.numel()
+    pipe = DeltaPipeline(spec, capacity=int(ci.size * 0.02), shards=sentinel_shards(spec))
+    pipe.step(p, m, v, wl.hp)
+    sync()
+    idx, val, total = pipe.delta()
+    assert total == want.idx.size
+    mapped = ci[idx]
+    order = np.argsort(mapped, kind="stable")
+    assert np.array_equal(mapped[order], want.idx)
+    assert np.array_equal(val[order], want.val)
+    check_buckets_and_shards(pipe, cplan, oremap.remap(cplan, want.idx, want.val))
+    pipe.close()
+    del pipe, p, m, v
+    torch.cuda.empty_cache()

@@ -57,3 +57,16 @@ def test_workload_sizes():
     for layer in range(12):
         roles = [t for t in moe.tensors if t.layer == layer and t.role == "expert_up"]
         assert sum(not t.touched for t in roles) == 96
+
+
+def test_2d_fill_equals_slices_of_the_canonical_draw():
+    rows, cols = 37, 53
+    full = synth.draw_cpu(rows * cols, 99, 5, 1).reshape(rows, cols)
+    out = np.full((40, 30), np.float32(-7.0))
+    # a 9 x 11 block of the canonical tensor at (12, 20) written into rows
+    # 3.. of a wider buffer (row stride 30) at column 4
+    synth.fill_cpu_2d(out[3:12, 4:15], 99, 5, 1, 12, 20, cols)
+    assert np.array_equal(out[3:12, 4:15].view(np.uint32), full[12:21, 20:31].view(np.uint32))
+    untouched = np.ones(out.shape, bool)
+    untouched[3:12, 4:15] = False
+    assert np.all(out[untouched] == np.float32(-7.0))

@@ -146,6 +146,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen3_8b_tp4")
     ap.add_argument("--lr", type=float, default=None)
+    ap.add_argument("--norm-group", action="store_true",
+                    help="norms in a parameter group without weight decay")
     ap.add_argument("--capacity-fraction", type=float, default=None,
                     help="delta buffer size as a fraction of the elements (default 0.02, "
                          "0.25 for the learning-rate sweep)")
@@ -163,12 +165,15 @@ def main():
     import torch
 
     from paper_2608_00455_amd import layouts
-    from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state
+    from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state, group_runs
+    from synth import workloads as W
 
     torch.cuda.set_device(0)
     if args.copy_calibration > 0:
         return copy_calibration(args.copy_calibration)
     wl = workload(args.workload, args.lr)
+    if args.norm_group:
+        wl = W.with_norm_group(wl)
     hp = wl.hp if args.lr is None else type(wl.hp)(lr=args.lr)
     spec = layouts.build_spec(wl)
     n = spec.total                           # elements of the trainer shard
@@ -181,6 +186,7 @@ def main():
         frac = 0.25 if args.workload == "qwen3_8b_4l_tp4" else 0.02
     cap = max(1 << 20, int(n * frac))
     pipe = DeltaPipeline(spec, capacity=cap)
+    runs = group_runs(wl, hp)
     stream = torch.cuda.current_stream()
     apply_only = args.workload.endswith("_apply")
 
@@ -195,7 +201,10 @@ def main():
         pipe.reset()
         if ev:
             ev[0].record(stream)
-        pipe.extract(p, m, v, hp)
+        if len(runs) == 1:
+            pipe.extract(p, m, v, hp)
+        else:
+            pipe.extract_runs(p, m, v, runs)
         if ev:
             ev[1].record(stream)
         pipe.remap()
@@ -262,7 +271,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
-        "config": {"workload": wl.name, "elements": n, "changed": changed,
+        "config": {"workload": wl.name, "elements": n, "changed": changed, "extract_calls": len(runs),
                    "change_fraction": c, "receiver_ranks": len(counts),
                    "routed_entries": routed, "lr": hp.lr,
                    "step_algorithmic_bytes": step_bytes,

@@ -161,13 +161,13 @@ def extract(wl, hp=None, threads: int = 0) -> Result:
     (eq. aligned_conversion), BF16 comparison per canonical tensor
     (eq. canonical_delta_detection); kept are the changes to elements that
     the sender rank holds."""
-    hp = hp or wl.hp
-    sc = core.derive_scalars(hp)
+    scs = run.scalars(wl, hp)
     threads = threads or run.cpu_threads()
     begins = wl.flat_begins()
     P, r = wl.sender.tp, wl.sender.rank
     idx_parts, val_parts = [], []
     for u in units(wl):
+        sc = scs[u.tensors[0]]                # the tensors of a unit share a group
         p_c, m_c, v_c = [], [], []
         for k in u.tensors:
             t = wl.tensors[k]

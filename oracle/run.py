@@ -102,6 +102,12 @@ def windows(wl, max_window: int = 1 << 24, tensors=None) -> List[Window]:
     return out
 
 
+def scalars(wl, hp=None) -> List[core.Scalars]:
+    """Step scalars of every tensor, from its parameter group's
+    hyperparameters (the weight-decay coefficient is per group, sec. 3.1)."""
+    return [core.derive_scalars(wl.group_hp(k, hp)) for k in range(len(wl.tensors))]
+
+
 @dataclass
 class Result:
     idx: np.ndarray
@@ -114,16 +120,15 @@ class Result:
 def extract(wl, hp=None, wins: Optional[List[Window]] = None, keep=(), threads: int = 0,
             max_window: int = 1 << 24) -> Result:
     """Detection over the given windows (default: the whole trainer shard)."""
-    hp = hp or wl.hp
-    sc = core.derive_scalars(hp)
+    sc = scalars(wl, hp)
     wins = wins if wins is not None else windows(wl, max_window)
     threads = threads or synth.default_threads()
     t0 = time.perf_counter()
     if threads <= 1 or len(wins) <= 1:
-        parts = [run_window(wl, w, sc, keep, threads=max(1, threads)) for w in wins]
+        parts = [run_window(wl, w, sc[w.tensor], keep, threads=max(1, threads)) for w in wins]
     else:
         with ThreadPoolExecutor(threads) as ex:
-            parts = list(ex.map(lambda w: run_window(wl, w, sc, keep), wins))
+            parts = list(ex.map(lambda w: run_window(wl, w, sc[w.tensor], keep), wins))
     diag = Diagnostics()
     for r in parts:
         diag.add(r.diag)

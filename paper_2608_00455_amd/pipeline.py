@@ -89,9 +89,22 @@ class DeltaPipeline:
                     [t.data_ptr() for t in self.off], [t.data_ptr() for t in self.rval],
                     self.rank_count.data_ptr(), self.rank_capacity, _stream(stream))
 
-    def step(self, p, m, v, hp, stream=None):
+    def extract_runs(self, p, m, v, runs, out_prev=None, stream=None):
+        """One dte_extract_delta per run (begin, end, hp) of the flat shard,
+        appending to the same delta (parameter groups, sec. 3.1)."""
+        for b, e, hp in runs:
+            self.extract(p[b:e], m[b:e], v[b:e], hp, n=e - b, index_base=b,
+                         out_prev=out_prev[b:e] if out_prev is not None else None,
+                         stream=stream)
+
+    def step(self, p, m, v, hp, stream=None, runs=None):
+        """reset, extract (over `runs` when the shard has several parameter
+        groups), remap, apply."""
         self.reset(stream)
-        self.extract(p, m, v, hp, stream=stream)
+        if runs is None:
+            self.extract(p, m, v, hp, stream=stream)
+        else:
+            self.extract_runs(p, m, v, runs, stream=stream)
         self.remap(stream)
         self.apply(stream)
 
@@ -180,10 +193,38 @@ def generate_state(wl, hp=None, device="cuda"):
                                       wl.seed, sp.tensor, kind, sp.canon_lo[0], sp.canon_lo[1],
                                       t.shape[1], s)
         begin += numel
-    B.dte_adamw_forward(p.data_ptr(), m.data_ptr(), v.data_ptr(), g.data_ptr(), n, hp, s)
+    for b, e, h in group_runs(wl, hp):
+        B.dte_adamw_forward(p[b:].data_ptr(), m[b:].data_ptr(), v[b:].data_ptr(),
+                            g[b:].data_ptr(), e - b, h, s)
     torch.cuda.current_stream().synchronize()
     del g
     return p, m, v
+
+
+def group_runs(wl, hp=None):
+    """Maximal runs [begin, end) of consecutive sender segments whose
+    parameter groups derive bit-identical step scalars, with the group's
+    hyperparameters: one extract call per run.  Without parameter groups,
+    or where the groups' scalars coincide (at small learning rates the
+    decay factor rounds to 1 whatever the weight decay), this is one run
+    over the whole shard."""
+    from .layouts import sender_segments
+
+    hp = hp or wl.hp
+    runs = []
+    begin = 0
+    for sg in sender_segments(wl):
+        numel = 1
+        for x in sg.shape:
+            numel *= x
+        h = wl.group_hp(sg.pieces[0].tensor, hp)
+        key = bytes(B.dte_derive_scalars(h))
+        if runs and runs[-1][3] == key:
+            runs[-1][1] = begin + numel
+        else:
+            runs.append([begin, begin + numel, h, key])
+        begin += numel
+    return [(b, e, h) for b, e, h, _ in runs]
 
 
 def spec_for(wl) -> PlanSpec:

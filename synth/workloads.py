@@ -17,7 +17,7 @@ states of the same shapes stand in for them.
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass, field, replace
 from typing import Optional, Tuple
 
 # Draw kinds (third Philox counter word).
@@ -127,6 +127,16 @@ class Workload:
     receiver: Receiver
     sweep_lr: Tuple[float, ...] = field(default_factory=tuple)
     sender: Sender = field(default_factory=Sender)
+    # Two parameter groups: the 1-D tensors (norms) without weight decay,
+    # the rest with hp.weight_decay.
+    no_decay_norms: bool = False
+
+    def group_hp(self, k: int, hp: Optional[StepHP] = None) -> StepHP:
+        """Step hyperparameters of the parameter group holding tensor k."""
+        hp = hp or self.hp
+        if self.no_decay_norms and len(self.tensors[k].shape) == 1:
+            return replace(hp, weight_decay=0.0)
+        return hp
 
     @property
     def numel(self) -> int:
@@ -343,11 +353,17 @@ def scaled_mcore(layers: int = 2, trainer_tp: int = 2, trainer_rank: int = 0,
 
 def with_sender_rank(wl: Workload, rank: int) -> Workload:
     """The same workload seen from another trainer TP rank."""
-    return Workload(wl.name, wl.description, wl.seed, wl.dims, wl.tensors, wl.hp, wl.receiver,
-                    wl.sweep_lr, Sender(wl.sender.kind, wl.sender.tp, rank))
+    return replace(wl, sender=Sender(wl.sender.kind, wl.sender.tp, rank))
 
 
 def canonical_twin(wl: Workload) -> Workload:
     """The same model state with the canonical sender layout."""
-    return Workload(wl.name + "_canonical", wl.description + " (canonical layout)", wl.seed,
-                    wl.dims, wl.tensors, wl.hp, wl.receiver, wl.sweep_lr, Sender())
+    return replace(wl, name=wl.name + "_canonical",
+                   description=wl.description + " (canonical layout)", sender=Sender())
+
+
+def with_norm_group(wl: Workload) -> Workload:
+    """The same workload with the norms in a parameter group of their own
+    (weight decay 0)."""
+    return replace(wl, name=wl.name + "_nd", description=wl.description + ", norms without decay",
+                   no_decay_norms=True)

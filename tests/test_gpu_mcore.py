@@ -21,7 +21,7 @@ from oracle import plan as oplan
 from oracle import remap as oremap
 from oracle import run as orun
 from paper_2608_00455_amd import layouts
-from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state
+from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state, group_runs
 from synth import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -60,6 +60,8 @@ MCORE = [
     lambda: W.scaled_mcore(layers=3, trainer_tp=2, trainer_rank=0, receiver_tp=8, hidden=256,
                            heads_q=16, heads_kv=8, head_dim=32, intermediate=704, vocab=512,
                            lr=1e-4),
+    # norms in a parameter group without weight decay: one extract per run
+    lambda: W.with_norm_group(W.scaled_mcore(trainer_rank=1, vocab=64, lr=1e-4)),
 ]
 
 
@@ -79,7 +81,7 @@ def check_mcore_path(wl, capacity_fraction=1.0):
     pipe = DeltaPipeline(spec, capacity=cap, shards=[dev(x.view(np.int16)) for x in old])
     p, m, v = generate_state(wl)
     assert p.numel() == ci.size
-    pipe.step(p, m, v, wl.hp)
+    pipe.step(p, m, v, wl.hp, runs=group_runs(wl))
     torch.cuda.synchronize()
     idx, val, total = pipe.delta()
     assert total == want.idx.size

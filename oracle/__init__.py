@@ -12,7 +12,11 @@ Modules, each following the paper's passage named in its header:
   plan   -- transfer plan T (sec. 3.2.2) for the receiver layouts
   remap  -- unravel / containment / ravel (sec. 3.2.2) and direct sparse
             apply (sec. 3.3, eq. direct_sparse_apply)
-  run    -- whole-workload driver (seeded state, forward step, detection)
+  run    -- whole-workload driver (seeded state, forward step, detection;
+            per-group step scalars, sec. 3.1)
+  mcore  -- Megatron-Core sender layout and converter (appendix B,
+            eq. mcore_fused_qkv, eq. mcore_tp_shard, eq. qkv_converter):
+            detection in the paper's order for one trainer TP rank
 
 Pins (tests/test_oracle_*.py) tie every function to the paper and to
 mathematics outside this package.  Parity unpinned: the change fraction and

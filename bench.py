@@ -146,6 +146,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen3_8b_tp4")
     ap.add_argument("--lr", type=float, default=None)
+    ap.add_argument("--ordered", action="store_true",
+                    help="dte_extract_delta_ordered (ascending, deterministic delta)")
     ap.add_argument("--norm-group", action="store_true",
                     help="norms in a parameter group without weight decay")
     ap.add_argument("--capacity-fraction", type=float, default=None,
@@ -185,7 +187,7 @@ def main():
     if frac is None:
         frac = 0.25 if args.workload == "qwen3_8b_4l_tp4" else 0.02
     cap = max(1 << 20, int(n * frac))
-    pipe = DeltaPipeline(spec, capacity=cap)
+    pipe = DeltaPipeline(spec, capacity=cap, ordered=args.ordered)
     runs = group_runs(wl, hp)
     stream = torch.cuda.current_stream()
     apply_only = args.workload.endswith("_apply")
@@ -272,6 +274,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
         "config": {"workload": wl.name, "elements": n, "changed": changed, "extract_calls": len(runs),
+                   "ordered": bool(args.ordered),
                    "change_fraction": c, "receiver_ranks": len(counts),
                    "routed_entries": routed, "lr": hp.lr,
                    "step_algorithmic_bytes": step_bytes,

@@ -105,13 +105,39 @@ dte_status dte_derive_scalars(const dte_adamw_step* hp, dte_scalars* out);
  *           synchronisation, *cursor > capacity means the delta is
  *           incomplete and must be recomputed with capacity >= *cursor.
  * out_prev: device binary32[n] receiving theta_hat, or NULL (no write).
- * Entry order is unspecified (the set of entries is exact); offsets are
- * unique within one call.  Errors: DTE_ERR_ARG (null pointer with n > 0,
+ * Entry order is unspecified (the set of entries is exact; each wave of the
+ * kernel writes its entries in ascending runs); offsets are unique within
+ * one call; dte_extract_delta_ordered gives ascending order.  Errors: DTE_ERR_ARG (null pointer with n > 0,
  * n < 0, index_base < 0, capacity < 0, invalid hp), DTE_ERR_HIP. */
 dte_status dte_extract_delta(const float* p, const float* m, const float* v, int64_t n,
                              int64_t index_base, const dte_adamw_step* hp, int64_t* out_idx,
                              uint16_t* out_val, int64_t capacity, int64_t* cursor,
                              float* out_prev, void* stream);
+
+/* Bytes of device workspace that dte_extract_delta_ordered needs for a
+ * given capacity (about 10 bytes per entry of capacity plus a fixed
+ * 256 KB); -1 if capacity is negative or above 2^40. */
+int64_t dte_ordered_workspace_bytes(int64_t capacity);
+
+/* dte_extract_delta with the entries in ascending offset order (paper
+ * sec. 3.2.2 asks for an ordered sparse payload per sender-receiver pair):
+ * the same set of entries, written to out_idx / out_val at positions
+ * *cursor, *cursor + 1, ... sorted by offset, and the same cursor
+ * semantics.  The order does not depend on timing: repeated calls on the
+ * same input write identical bytes.  Successive calls on ascending
+ * sub-ranges (parameter groups) keep the whole delta ascending.
+ * workspace: device memory of at least dte_ordered_workspace_bytes(capacity)
+ *            bytes, 256-byte aligned, owned by the caller, not read by the
+ *            caller afterwards; calls that overlap on one workspace race.
+ * If the true total exceeds capacity the output holds an unspecified
+ * subset (recompute with capacity >= *cursor - entry value).
+ * Errors: as dte_extract_delta; DTE_ERR_ARG also for a missing, small or
+ * misaligned workspace. */
+dte_status dte_extract_delta_ordered(const float* p, const float* m, const float* v, int64_t n,
+                                     int64_t index_base, const dte_adamw_step* hp,
+                                     int64_t* out_idx, uint16_t* out_val, int64_t capacity,
+                                     int64_t* cursor, void* workspace, int64_t workspace_bytes,
+                                     float* out_prev, void* stream);
 
 /* One canonical parameter of the flat trainer shard (paper sec. 3.2.2:
  * sender-local converted tensor of shape n_s): flat_begin is its offset in

@@ -15,7 +15,8 @@ DTE_OK, DTE_ERR_ARG, DTE_ERR_PLAN, DTE_ERR_CAPACITY, DTE_ERR_HIP = 0, 1, 2, 3, 4
 DTE_MAX_DIMS = 4
 DTE_MAX_RANKS = 64
 
-EXPORTED = ("dte_derive_scalars", "dte_extract_delta", "dte_plan_create", "dte_plan_destroy",
+EXPORTED = ("dte_derive_scalars", "dte_extract_delta", "dte_ordered_workspace_bytes",
+            "dte_extract_delta_ordered", "dte_plan_create", "dte_plan_destroy",
             "dte_plan_info", "dte_remap", "dte_apply", "dte_adamw_forward", "dte_status_string")
 
 
@@ -69,6 +70,12 @@ def _lib():
         L.dte_extract_delta.restype = S
         L.dte_extract_delta.argtypes = [P, P, P, I64, I64, ctypes.POINTER(dte_adamw_step), P, P,
                                         I64, P, P, P]
+        L.dte_ordered_workspace_bytes.restype = I64
+        L.dte_ordered_workspace_bytes.argtypes = [I64]
+        L.dte_extract_delta_ordered.restype = S
+        L.dte_extract_delta_ordered.argtypes = [P, P, P, I64, I64,
+                                                ctypes.POINTER(dte_adamw_step), P, P, I64, P, P,
+                                                I64, P, P]
         L.dte_plan_create.restype = S
         L.dte_plan_create.argtypes = [ctypes.POINTER(dte_segment), I32, ctypes.POINTER(dte_op),
                                       I32, I32, ctypes.POINTER(I64), ctypes.POINTER(P)]
@@ -124,6 +131,19 @@ def dte_extract_delta(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cu
     _check("dte_extract_delta",
            _lib().dte_extract_delta(p, m, v, n, index_base, ctypes.byref(_hp(hp)), out_idx,
                                     out_val, capacity, cursor, out_prev or None, stream or None))
+
+
+def dte_ordered_workspace_bytes(capacity) -> int:
+    return int(_lib().dte_ordered_workspace_bytes(capacity))
+
+
+def dte_extract_delta_ordered(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cursor,
+                              workspace, workspace_bytes, out_prev=0, stream=0):
+    _check("dte_extract_delta_ordered",
+           _lib().dte_extract_delta_ordered(p, m, v, n, index_base, ctypes.byref(_hp(hp)),
+                                            out_idx, out_val, capacity, cursor,
+                                            workspace or None, workspace_bytes,
+                                            out_prev or None, stream or None))
 
 
 def dte_adamw_forward(p, m, v, g, n, hp, stream=0):

@@ -277,19 +277,27 @@ dte_status dte_derive_scalars(const dte_adamw_step* hp, dte_scalars* out)
     return DTE_OK;
 }
 
-dte_status dte_extract_delta(const float* p, const float* m, const float* v, int64_t n,
-                             int64_t index_base, const dte_adamw_step* hp, int64_t* out_idx,
-                             uint16_t* out_val, int64_t capacity, int64_t* cursor,
-                             float* out_prev, void* stream)
+namespace {
+
+bool extract_args_ok(const float* p, const float* m, const float* v, int64_t n,
+                     int64_t index_base, const dte_adamw_step* hp, int64_t* out_idx,
+                     uint16_t* out_val, int64_t capacity, int64_t* cursor)
 {
-    if (n < 0 || index_base < 0 || capacity < 0 || !valid_hp(hp) || !bias_ok(*hp))
-        return DTE_ERR_ARG;
-    if (n == 0) return DTE_OK;
-    if (!p || !m || !v || !cursor) return DTE_ERR_ARG;
-    if (capacity > 0 && (!out_idx || !out_val)) return DTE_ERR_ARG;
-    if (index_base > INT64_MAX - n) return DTE_ERR_ARG;
+    if (n < 0 || index_base < 0 || capacity < 0 || !valid_hp(hp) || !bias_ok(*hp)) return false;
+    if (n == 0) return true;
+    if (!p || !m || !v || !cursor) return false;
+    if (capacity > 0 && (!out_idx || !out_val)) return false;
+    if (index_base > INT64_MAX - n) return false;
+    return true;
+}
+
+dte::ExtractParams extract_params(const float* p, const float* m, const float* v, int64_t n,
+                                  int64_t index_base, const dte_adamw_step* hp,
+                                  int64_t* out_idx, uint16_t* out_val, int64_t capacity,
+                                  int64_t* cursor, float* out_prev)
+{
     const AllScalars sc = derive(*hp);
-    dte::ExtractParams a;
+    dte::ExtractParams a{};
     a.p = p;
     a.m = m;
     a.v = v;
@@ -311,8 +319,103 @@ dte_status dte_extract_delta(const float* p, const float* m, const float* v, int
     a.capacity = capacity;
     a.cursor = cursor;
     a.out_prev = out_prev;
+    a.runs = nullptr;
+    return a;
+}
+
+// Ordered-mode workspace: unordered entries, run records, wave totals and
+// bases, two counters; every part 256-byte aligned.
+struct OrderedWorkspace {
+    int64_t idx, val, runs, wave_count, wave_base, counters, total;
+    int64_t max_runs;
+};
+
+int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+OrderedWorkspace ordered_layout(int64_t capacity)
+{
+    OrderedWorkspace w;
+    // every flush but a wave's last holds more than 768 entries (a flush
+    // happens when at most 256 more would overflow 1024 staged entries)
+    w.max_runs = capacity / 769 + dte::kMaxOrderedWaves + 1;
+    w.idx = 0;
+    w.val = align256(w.idx + capacity * (int64_t)sizeof(int64_t));
+    w.runs = align256(w.val + capacity * (int64_t)sizeof(uint16_t));
+    w.wave_count = align256(w.runs + w.max_runs * (int64_t)sizeof(dte::OrderRun));
+    w.wave_base = align256(w.wave_count + dte::kMaxOrderedWaves * (int64_t)sizeof(int64_t));
+    w.counters = align256(w.wave_base + dte::kMaxOrderedWaves * (int64_t)sizeof(int64_t));
+    w.total = align256(w.counters + 2 * (int64_t)sizeof(int64_t));
+    return w;
+}
+
+}  // namespace
+
+dte_status dte_extract_delta(const float* p, const float* m, const float* v, int64_t n,
+                             int64_t index_base, const dte_adamw_step* hp, int64_t* out_idx,
+                             uint16_t* out_val, int64_t capacity, int64_t* cursor,
+                             float* out_prev, void* stream)
+{
+    if (!extract_args_ok(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cursor))
+        return DTE_ERR_ARG;
+    if (n == 0) return DTE_OK;
+    const dte::ExtractParams a = extract_params(p, m, v, n, index_base, hp, out_idx, out_val,
+                                                capacity, cursor, out_prev);
     return dte::launch_extract(a, current_cus(), (hipStream_t)stream) == hipSuccess ? DTE_OK
                                                                                      : DTE_ERR_HIP;
+}
+
+int64_t dte_ordered_workspace_bytes(int64_t capacity)
+{
+    if (capacity < 0 || capacity > ((int64_t)1 << 40)) return -1;
+    return ordered_layout(capacity).total;
+}
+
+dte_status dte_extract_delta_ordered(const float* p, const float* m, const float* v, int64_t n,
+                                     int64_t index_base, const dte_adamw_step* hp,
+                                     int64_t* out_idx, uint16_t* out_val, int64_t capacity,
+                                     int64_t* cursor, void* workspace, int64_t workspace_bytes,
+                                     float* out_prev, void* stream)
+{
+    if (!extract_args_ok(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cursor))
+        return DTE_ERR_ARG;
+    if (n == 0) return DTE_OK;
+    const int64_t need = dte_ordered_workspace_bytes(capacity);
+    if (need < 0 || !workspace || workspace_bytes < need ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return DTE_ERR_ARG;
+    const OrderedWorkspace w = ordered_layout(capacity);
+    char* base = static_cast<char*>(workspace);
+    int64_t* counters = reinterpret_cast<int64_t*>(base + w.counters);
+    const hipStream_t s = (hipStream_t)stream;
+    const int cus = current_cus();
+    // unordered fill level and run count start at zero (a fill kernel)
+    if (dte::launch_zero_i64(counters, 2, s) != hipSuccess) return DTE_ERR_HIP;
+    dte::ExtractParams a = extract_params(p, m, v, n, index_base, hp,
+                                          reinterpret_cast<int64_t*>(base + w.idx),
+                                          reinterpret_cast<uint16_t*>(base + w.val), capacity,
+                                          counters, out_prev);
+    a.runs = reinterpret_cast<dte::OrderRun*>(base + w.runs);
+    a.max_runs = w.max_runs;
+    a.run_cursor = counters + 1;
+    a.wave_count = reinterpret_cast<int64_t*>(base + w.wave_count);
+    int32_t waves = 0;
+    if (dte::launch_extract(a, cus, s, &waves) != hipSuccess) return DTE_ERR_HIP;
+    dte::OrderParams o;
+    o.runs = a.runs;
+    o.run_cursor = a.run_cursor;
+    o.max_runs = w.max_runs;
+    o.wave_count = a.wave_count;
+    o.wave_base = reinterpret_cast<int64_t*>(base + w.wave_base);
+    o.waves = waves;
+    o.src_idx = a.out_idx;
+    o.src_val = a.out_val;
+    o.unordered_total = counters;
+    o.src_capacity = capacity;
+    o.out_idx = out_idx;
+    o.out_val = out_val;
+    o.capacity = capacity;
+    o.cursor = cursor;
+    return dte::launch_order(o, cus, s) == hipSuccess ? DTE_OK : DTE_ERR_HIP;
 }
 
 dte_status dte_adamw_forward(float* p, float* m, float* v, const float* g, int64_t n,

@@ -11,11 +11,21 @@ namespace dte {
 
 // ---- extract (fused AdamW inverse + BF16 detection + compaction) --------
 
+// One flush of one wave in ordered mode: `count` entries written at
+// unordered position `src`, preceded in the wave's ascending output by
+// `woff` entries of earlier flushes.
+struct OrderRun {
+    int64_t src;
+    int64_t woff;
+    int32_t count;
+    int32_t wave;         // global wave number (launch order)
+};
+
 struct ExtractParams {
     const float* p;
     const float* m;
     const float* v;
-    int64_t n;            // elements of this launch
+    int64_t n;            // elements of this call
     int64_t index_base;   // flat trainer offset of element 0
     float lrb1, rbc2, eps, decay;
     float rd_lo, rd_hi;   // binary32 bracket of 1/decay: rd_lo <= 1/decay <= rd_hi
@@ -24,9 +34,45 @@ struct ExtractParams {
     int64_t capacity;
     int64_t* cursor;
     float* out_prev;      // nullable
+    // ordered mode (runs != nullptr): every flush is recorded, every wave
+    // writes its entry total to wave_count[wave]
+    OrderRun* runs;
+    int64_t max_runs;
+    int64_t* run_cursor;
+    int64_t* wave_count;
+    int32_t wave0;        // global number of this launch's first wave
 };
 
-hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream);
+// Largest number of waves one extract call launches in ordered mode.
+constexpr int kMaxOrderedWaves = 16384;
+
+// Launches the extract kernels; *waves receives the number of waves
+// launched (the global wave numbers are 0 .. *waves - 1).
+hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream,
+                          int32_t* waves = nullptr);
+
+// Ordered mode, after launch_extract: wave_base[g] = *cursor + entries of
+// waves < g; copies every recorded run from the unordered arrays to
+// (out_idx, out_val) at wave_base[run.wave] + run.woff (positions below
+// capacity); then *cursor += *unordered_total.
+struct OrderParams {
+    const OrderRun* runs;
+    const int64_t* run_cursor;
+    int64_t max_runs;
+    const int64_t* wave_count;
+    int64_t* wave_base;
+    int32_t waves;
+    const int64_t* src_idx;
+    const uint16_t* src_val;
+    const int64_t* unordered_total;
+    int64_t src_capacity;
+    int64_t* out_idx;
+    uint16_t* out_val;
+    int64_t capacity;
+    int64_t* cursor;
+};
+
+hipError_t launch_order(const OrderParams& o, int cus, hipStream_t stream);
 
 struct ForwardParams {
     float* p;

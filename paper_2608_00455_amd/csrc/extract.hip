@@ -5,9 +5,9 @@
 //
 // Design (HBM-bound: 12 bytes read per element, ~10 bytes written per
 // changed element):
-//  - persistent grid (3 blocks of 4 waves per CU); each block owns one
-//    contiguous range of 2048-element tiles and its waves take every fourth
-//    tile of it (so entries leave each wave as local, ascending runs);
+//  - persistent grid (3 blocks of 4 waves per CU); each wave owns one
+//    contiguous range of 2048-element tiles, ranges ascending with the
+//    global wave number, so every wave's entries leave in ascending order;
 //    a wave loads eight float4 of p, m and v per lane, i.e. 24 16-byte
 //    non-temporal loads in flight per lane, which is what keeps the HBM
 //    queues full at this occupancy;
@@ -23,13 +23,21 @@
 //    time with the correctly rounded inverse.  The result is bit-identical
 //    to evaluating every element exactly.  When theta_hat is requested every
 //    element takes the exact path;
-//  - the change predicate of 64 elements is one ballot; a lane's staging
-//    slot is the running count plus mbcnt within the ballot; changed entries
-//    (packed 32-bit position + BF16 value) are staged per wave in LDS and a
-//    wave reserves global output space with one atomicAdd on the 64-bit
-//    cursor per flush of its staging area (1024 entries), then writes the
-//    entries out coalesced.  No block-wide barrier anywhere; the number of
-//    atomics is bounded by entries / 1024 + waves.
+//  - the predicate of one float4 slot of the wave (256 consecutive
+//    elements) is four ballots; an element's position among the slot's
+//    selected elements is the sum of mbcnt over the four ballots (lanes
+//    before it) plus its own selected predecessors in the lane, so
+//    candidates are queued, and changed entries (packed 32-bit position +
+//    BF16 value) staged in LDS, in ascending element order: every wave's
+//    output is ascending.  A wave reserves global output space with one
+//    atomicAdd on the 64-bit cursor per flush of its staging area (1024
+//    entries), then writes the entries out coalesced.  No block-wide barrier anywhere; the number of
+//    atomics is bounded by entries / 1024 + waves;
+//  - ordered mode: each flush also records (unordered position, entries of
+//    the wave before it, count, wave) and each wave its total; a scan of the
+//    wave totals and a copy of the recorded runs then give the entries in
+//    ascending offset order (order_kernel below), deterministic whatever
+//    the timing of the atomics.
 #include <hip/hip_runtime.h>
 
 #include "dte_internal.h"
@@ -45,8 +53,8 @@ constexpr int kVec = 8;                       // float4 per lane per array per t
 constexpr int kSlots = 4 * kVec;              // elements per lane per tile
 constexpr int kWaveTile = 64 * kSlots;        // 1024 elements per wave tile
 constexpr int kWaveStage = 1024;              // staged output entries per wave (6 bytes each)
-constexpr int kQueue = 128;                   // queued candidates per wave (16 bytes each)
-constexpr int kBlocksPerCU = 3;               // 3 waves per SIMD (VGPR-bound), 32 KB LDS
+constexpr int kQueue = 256;                   // queued candidates per wave (16 bytes each)
+constexpr int kBlocksPerCU = 3;               // 3 waves per SIMD (VGPR-bound), 40 KB LDS
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -131,7 +139,7 @@ __device__ __forceinline__ float exact_prev(float p, float m, float v, const Ext
 constexpr int kTileBits = __builtin_ctz(kWaveTile);
 static_assert((1 << kTileBits) == kWaveTile, "wave tile must be a power of two");
 // Per-wave LDS areas.  Keys are (wave iteration << kTileBits) | element in
-// the tile; the wave's tiles are t_first + iteration * nwaves.
+// the tile; the wave's tiles are t_first + iteration.
 struct WaveStage {
     uint32_t* key;    // output staging: changed entries awaiting a flush
     uint16_t* val;
@@ -140,7 +148,13 @@ struct WaveStage {
     float* qv;
     uint32_t* qkey;
     int64_t t_first;
-    int64_t nwaves;
+    int32_t wave;     // global wave number
+};
+
+// Wave-uniform output state: entries staged in LDS, entries flushed so far.
+struct Staging {
+    int staged;
+    int64_t flushed;
 };
 
 __device__ __forceinline__ void wave_sync()
@@ -150,52 +164,96 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Copy a wave's `staged` LDS entries to the reserved global range.
-__device__ void flush_wave(const ExtractParams& a, const WaveStage& st, int staged, int lane)
+// Copy a wave's staged LDS entries to the reserved global range (and, in
+// ordered mode, record the run).
+__device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging& so, int lane)
 {
+    const int staged = so.staged;
     wave_sync();   // every lane's LDS stores visible to the other lanes
     unsigned long long base = 0;
-    if (lane == 0)
+    if (lane == 0) {
         base = atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor),
                          (unsigned long long)staged);
+        if (a.runs) {
+            const unsigned long long r =
+                atomicAdd(reinterpret_cast<unsigned long long*>(a.run_cursor), 1ull);
+            if ((int64_t)r < a.max_runs) {
+                OrderRun run;
+                run.src = (int64_t)base;
+                run.woff = so.flushed;
+                run.count = staged;
+                run.wave = st.wave;
+                a.runs[r] = run;
+            }
+        }
+    }
     base = __shfl(base, 0);
     for (int i = lane; i < staged; i += 64) {
         const int64_t pos = (int64_t)base + i;
         if (pos < a.capacity) {
             const uint32_t key = st.key[i];
-            const int64_t t = st.t_first + (int64_t)(key >> kTileBits) * st.nwaves;
+            const int64_t t = st.t_first + (int64_t)(key >> kTileBits);
             a.out_idx[pos] = a.index_base + t * kWaveTile + (key & (kWaveTile - 1));
             a.out_val[pos] = st.val[i];
         }
     }
+    so.flushed += staged;
+    so.staged = 0;
     wave_sync();   // the staging area is rewritten next: finish these reads first
+}
+
+// Selection of the four elements of each lane's float4 slot (256
+// consecutive elements per wave): one ballot per element of the float4 and
+// the slot's count.
+struct Slot4 {
+    uint64_t ball[4];
+    int count;
+};
+
+__device__ __forceinline__ Slot4 select4(const bool (&sel)[4])
+{
+    Slot4 r;
+    r.count = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        r.ball[c] = __ballot(sel[c]);
+        r.count += __popcll(r.ball[c]);
+    }
+    return r;
+}
+
+// Selected elements of the slot in lanes below this one: the position of
+// this lane's first selected element; its others follow in element order.
+__device__ __forceinline__ int lanes_before(const Slot4& r)
+{
+    int before = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) before += lane_prefix(r.ball[k]);
+    return before;
 }
 
 // Stage one ballot of changed entries (at most 64), flushing first when the
 // staging area would overflow.  Wave-uniform control flow.
 __device__ __forceinline__ void stage_changed(const ExtractParams& a, const WaveStage& st,
-                                              int& staged, int lane, bool changed,
+                                              Staging& so, int lane, bool changed,
                                               uint32_t key, uint16_t val)
 {
     const uint64_t k = __ballot(changed);
     if (k == 0) return;
     const int cnt = __popcll(k);
-    if (staged + cnt > kWaveStage) {
-        flush_wave(a, st, staged, lane);
-        staged = 0;
-    }
+    if (so.staged + cnt > kWaveStage) flush_wave(a, st, so, lane);
     if (changed) {
-        const int pos = staged + lane_prefix(k);
+        const int pos = so.staged + lane_prefix(k);
         st.key[pos] = key;
         st.val[pos] = val;
     }
-    staged += cnt;
+    so.staged += cnt;
 }
 
 // Exact inverse of every queued candidate, 64 per pass; changed ones are
 // staged.  Empties the queue.
 template <bool kDecayOne>
-__device__ void drain_queue(const ExtractParams& a, const WaveStage& st, int& queued, int& staged,
+__device__ void drain_queue(const ExtractParams& a, const WaveStage& st, int& queued, Staging& so,
                             int lane)
 {
     wave_sync();
@@ -211,7 +269,7 @@ __device__ void drain_queue(const ExtractParams& a, const WaveStage& st, int& qu
             changed = bf16_bits(ph) != bn;
             key = st.qkey[i];
         }
-        stage_changed(a, st, staged, lane, changed, key, bn);
+        stage_changed(a, st, so, lane, changed, key, bn);
     }
     queued = 0;
     wave_sync();
@@ -244,7 +302,7 @@ __device__ __forceinline__ void load_tile(const ExtractParams& a, int64_t t0, in
 
 template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev>
 __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0, int lane,
-                                             int& staged, int& queued, const WaveStage& st,
+                                             Staging& so, int& queued, const WaveStage& st,
                                              uint32_t iter, const f32x4* P, const f32x4* M,
                                              const f32x4* V)
 {
@@ -252,42 +310,64 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
 #pragma unroll
     for (int j = 0; j < kVec; ++j) {
         const int off = (j * 64 + lane) * 4;
-        f32x4 prev;
+        const uint32_t key0 = (iter << kTileBits) | (uint32_t)off;
+        if (kWritePrev) {
+            // theta_hat requested: the exact path for every element
+            f32x4 prev;
+            bool sel[4];
+            uint32_t bn[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float p = P[j][c];
-            const bool in = kFull || (off + c < rem);
-            const uint32_t key = (iter << kTileBits) | (uint32_t)(off + c);
-            if (kWritePrev) {
-                // theta_hat requested: the exact path for every element
+            for (int c = 0; c < 4; ++c) {
+                const float p = P[j][c];
                 const float ph = exact_prev<kDecayOne>(p, M[j][c], V[j][c], a);
                 prev[c] = ph;
-                const uint32_t bn = bf16_bits(p);
-                stage_changed(a, st, staged, lane, in && bf16_bits(ph) != bn, key, (uint16_t)bn);
-            } else {
-                const bool cand = in && !proven_unchanged<kDecayOne>(p, M[j][c], V[j][c], a);
-                const uint64_t ck = __ballot(cand);
-                if (ck != 0) {
-                    const int cnt = __popcll(ck);
-                    if (queued + cnt > kQueue) drain_queue<kDecayOne>(a, st, queued, staged, lane);
-                    if (cand) {
-                        const int pos = queued + lane_prefix(ck);
-                        st.qp[pos] = p;
-                        st.qm[pos] = M[j][c];
-                        st.qv[pos] = V[j][c];
-                        st.qkey[pos] = key;
-                    }
-                    queued += cnt;
-                }
+                bn[c] = bf16_bits(p);
+                sel[c] = (kFull || off + c < rem) && bf16_bits(ph) != bn[c];
             }
-        }
-        if (kWritePrev) {
+            const Slot4 r = select4(sel);
+            if (r.count != 0) {
+                if (so.staged + r.count > kWaveStage) flush_wave(a, st, so, lane);
+                const int base = so.staged + lanes_before(r);
+                int k = 0;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    if (sel[c]) {
+                        st.key[base + k] = key0 + c;
+                        st.val[base + k] = (uint16_t)bn[c];
+                        ++k;
+                    }
+                }
+                so.staged += r.count;
+            }
             if (kFull || (kVecLoads && off + 3 < rem)) {
                 __builtin_nontemporal_store(prev, reinterpret_cast<f32x4*>(a.out_prev + t0 + off));
             } else {
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
                     if (off + c < rem) a.out_prev[t0 + off + c] = prev[c];
+            }
+        } else {
+            bool sel[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                sel[c] = (kFull || off + c < rem) &&
+                         !proven_unchanged<kDecayOne>(P[j][c], M[j][c], V[j][c], a);
+            const Slot4 r = select4(sel);
+            if (r.count != 0) {
+                if (queued + r.count > kQueue) drain_queue<kDecayOne>(a, st, queued, so, lane);
+                const int base = queued + lanes_before(r);
+                int k = 0;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    if (sel[c]) {
+                        st.qp[base + k] = P[j][c];
+                        st.qm[base + k] = M[j][c];
+                        st.qv[base + k] = V[j][c];
+                        st.qkey[base + k] = key0 + c;
+                        ++k;
+                    }
+                }
+                queued += r.count;
             }
         }
     }
@@ -307,26 +387,26 @@ __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    // block b owns the contiguous tile range [b per, (b+1) per); its waves
-    // take every kWaves-th tile of it, so the four waves of a block stream
-    // neighbouring tiles and each wave's output is a local, ascending run
-    const int64_t per = (last - first + gridDim.x - 1) / gridDim.x;
-    const int64_t b_first = first + (int64_t)blockIdx.x * per;
-    const int64_t b_last = (b_first + per < last) ? b_first + per : last;
-    int64_t t = b_first + wave;
-    int staged = 0;
+    // wave g of the launch owns the contiguous tile range [g per, (g+1) per)
+    const int64_t g = (int64_t)blockIdx.x * kWaves + wave;
+    const int64_t nw = (int64_t)gridDim.x * kWaves;
+    const int64_t per = (last - first + nw - 1) / nw;
+    const int64_t w_first = first + g * per;
+    const int64_t w_last = (w_first + per < last) ? w_first + per : last;
+    Staging so{0, 0};
     const WaveStage st{s_key[wave], s_val[wave], s_qp[wave], s_qm[wave], s_qv[wave],
-                       s_qkey[wave], t, kWaves};
+                       s_qkey[wave], w_first, a.wave0 + (int32_t)g};
     uint32_t iter = 0;
     int queued = 0;
-    for (; t < b_last; t += kWaves) {
+    for (int64_t t = w_first; t < w_last; ++t) {
         f32x4 P[kVec], M[kVec], V[kVec];
         load_tile<kFull, kVecLoads>(a, t * kWaveTile, lane, P, M, V);
-        process_tile<kFull, kVecLoads, kDecayOne, kWritePrev>(a, t * kWaveTile, lane, staged,
+        process_tile<kFull, kVecLoads, kDecayOne, kWritePrev>(a, t * kWaveTile, lane, so,
                                                              queued, st, iter++, P, M, V);
     }
-    if (queued > 0) drain_queue<kDecayOne>(a, st, queued, staged, lane);
-    if (staged > 0) flush_wave(a, st, staged, lane);
+    if (queued > 0) drain_queue<kDecayOne>(a, st, queued, so, lane);
+    if (so.staged > 0) flush_wave(a, st, so, lane);
+    if (a.runs && lane == 0) a.wave_count[st.wave] = so.flushed;
 }
 
 template <bool kVecLoads>
@@ -373,46 +453,115 @@ __global__ __launch_bounds__(256) void adamw_forward_kernel(ForwardParams a)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Launch over wave tiles [first, last); returns the number of waves.
 template <bool F, bool V, bool D>
-void launch_tiles(const ExtractParams& a, int64_t first, int64_t last, int64_t max_grid,
-                  hipStream_t s)
+int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_grid,
+                     int32_t wave0, hipStream_t s)
 {
-    if (last <= first) return;
+    if (last <= first) return 0;
     const int64_t blocks = (last - first + kWaves - 1) / kWaves;
     const dim3 grid((unsigned)(blocks < max_grid ? blocks : max_grid));
+    a.wave0 = wave0;
     if (a.out_prev)
         hipLaunchKernelGGL((extract_kernel<F, V, D, true>), grid, dim3(kBlock), 0, s, a, first,
                            last);
     else
         hipLaunchKernelGGL((extract_kernel<F, V, D, false>), grid, dim3(kBlock), 0, s, a, first,
                            last);
+    return (int32_t)grid.x * kWaves;
 }
 
 template <bool D>
-void launch_all(const ExtractParams& a, bool vec, int64_t max_grid, hipStream_t s)
+int32_t launch_all(const ExtractParams& a, bool vec, int64_t max_grid, hipStream_t s)
 {
     const int64_t full = a.n / kWaveTile;
     const int64_t ntiles = (a.n + kWaveTile - 1) / kWaveTile;
     if (vec) {
-        launch_tiles<true, true, D>(a, 0, full, max_grid, s);       // unguarded body
-        launch_tiles<false, true, D>(a, full, ntiles, max_grid, s); // ragged last tile
-    } else {
-        launch_tiles<false, false, D>(a, 0, ntiles, max_grid, s);   // scalar loads
+        const int32_t w = launch_tiles<true, true, D>(a, 0, full, max_grid, 0, s);  // unguarded
+        return w + launch_tiles<false, true, D>(a, full, ntiles, max_grid, w, s);   // ragged tail
+    }
+    return launch_tiles<false, false, D>(a, 0, ntiles, max_grid, 0, s);           // scalar loads
+}
+
+// ---- ordered mode: runs to ascending positions ----------------------------
+
+// One block: wave_base = *cursor + exclusive prefix of the wave totals; then
+// the cursor advances by the true total of the call.
+__global__ __launch_bounds__(1024) void order_scan_kernel(OrderParams o)
+{
+    constexpr int kThreads = 1024;
+    constexpr int kPer = kMaxOrderedWaves / kThreads;
+    __shared__ int64_t part[kThreads];
+    const int tid = threadIdx.x;
+    const int lo = tid * kPer;
+    int64_t sum = 0;
+    for (int i = 0; i < kPer; ++i)
+        if (lo + i < o.waves) sum += o.wave_count[lo + i];
+    part[tid] = sum;
+    __syncthreads();
+    for (int d = 1; d < kThreads; d <<= 1) {      // inclusive scan of the partial sums
+        const int64_t x = (tid >= d) ? part[tid - d] : 0;
+        __syncthreads();
+        part[tid] += x;
+        __syncthreads();
+    }
+    const int64_t c0 = *o.cursor;
+    int64_t run = c0 + part[tid] - sum;
+    for (int i = 0; i < kPer; ++i) {
+        if (lo + i < o.waves) {
+            o.wave_base[lo + i] = run;
+            run += o.wave_count[lo + i];
+        }
+    }
+    __syncthreads();                              // every thread has read the cursor
+    if (tid == 0) *o.cursor = c0 + *o.unordered_total;
+}
+
+// Each wave copies whole runs: entry i of a run moves from src + i to
+// wave_base[wave] + woff + i.
+__global__ __launch_bounds__(kBlock) void order_copy_kernel(OrderParams o)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+    const int64_t nw = (int64_t)gridDim.x * kWaves;
+    int64_t nruns = *o.run_cursor;
+    if (nruns > o.max_runs) nruns = o.max_runs;
+    for (int64_t r = w; r < nruns; r += nw) {
+        const OrderRun run = o.runs[r];
+        const int64_t dst0 = o.wave_base[run.wave] + run.woff;
+        for (int i = lane; i < run.count; i += 64) {
+            const int64_t src = run.src + i;
+            const int64_t dst = dst0 + i;
+            if (src < o.src_capacity && dst < o.capacity) {
+                o.out_idx[dst] = o.src_idx[src];
+                o.out_val[dst] = o.src_val[src];
+            }
+        }
     }
 }
 
 }  // namespace
 
-hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream)
+hipError_t launch_order(const OrderParams& o, int cus, hipStream_t stream)
 {
+    if (o.waves <= 0) return hipSuccess;
+    hipLaunchKernelGGL(order_scan_kernel, dim3(1), dim3(1024), 0, stream, o);
+    hipLaunchKernelGGL(order_copy_kernel, dim3((unsigned)cus * 4), dim3(kBlock), 0, stream, o);
+    return hipGetLastError();
+}
+
+hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream, int32_t* waves)
+{
+    if (waves) *waves = 0;
     if (a.n <= 0) return hipSuccess;
-    const int64_t max_grid = (int64_t)cus * kBlocksPerCU;
+    int64_t max_grid = (int64_t)cus * kBlocksPerCU;
+    // ordered mode: both launches together stay within kMaxOrderedWaves
+    if (a.runs && max_grid > kMaxOrderedWaves / kWaves - 1) max_grid = kMaxOrderedWaves / kWaves - 1;
     const bool vec = aligned16(a.p) && aligned16(a.m) && aligned16(a.v) &&
                      (a.out_prev == nullptr || aligned16(a.out_prev));
-    if (a.decay == 1.0f)
-        launch_all<true>(a, vec, max_grid, stream);
-    else
-        launch_all<false>(a, vec, max_grid, stream);
+    const int32_t w = (a.decay == 1.0f) ? launch_all<true>(a, vec, max_grid, stream)
+                                        : launch_all<false>(a, vec, max_grid, stream);
+    if (waves) *waves = w;
     return hipGetLastError();
 }
 

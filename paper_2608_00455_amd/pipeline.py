@@ -45,8 +45,10 @@ class Plan:
 
 class DeltaPipeline:
     def __init__(self, spec: PlanSpec, capacity: int, rank_capacity: Optional[List[int]] = None,
-                 device="cuda", shards: Optional[List[torch.Tensor]] = None):
+                 device="cuda", shards: Optional[List[torch.Tensor]] = None,
+                 ordered: bool = False):
         self.plan = Plan(spec)
+        self.ordered = ordered
         self.device = torch.device(device)
         self.capacity = int(capacity)
         R = self.plan.nranks
@@ -64,6 +66,10 @@ class DeltaPipeline:
             shards = [torch.zeros(max(1, n), dtype=torch.int16, device=self.device)
                       for n in spec.rank_numel]
         self.shards = shards
+        self.workspace = None
+        if ordered:
+            nbytes = B.dte_ordered_workspace_bytes(self.capacity)
+            self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
 
     # -- the three hot calls ------------------------------------------------
     def reset(self, stream=None):
@@ -73,10 +79,17 @@ class DeltaPipeline:
 
     def extract(self, p, m, v, hp, n=None, index_base=0, out_prev=None, stream=None):
         n = p.numel() if n is None else n
-        B.dte_extract_delta(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, index_base, hp,
-                            self.idx.data_ptr(), self.val.data_ptr(), self.capacity,
-                            self.cursor.data_ptr(),
-                            out_prev.data_ptr() if out_prev is not None else 0, _stream(stream))
+        prev = out_prev.data_ptr() if out_prev is not None else 0
+        if self.ordered:
+            B.dte_extract_delta_ordered(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, index_base,
+                                        hp, self.idx.data_ptr(), self.val.data_ptr(),
+                                        self.capacity, self.cursor.data_ptr(),
+                                        self.workspace.data_ptr(), self.workspace.numel(), prev,
+                                        _stream(stream))
+        else:
+            B.dte_extract_delta(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, index_base, hp,
+                                self.idx.data_ptr(), self.val.data_ptr(), self.capacity,
+                                self.cursor.data_ptr(), prev, _stream(stream))
 
     def remap(self, stream=None):
         B.dte_remap(self.plan.handle, self.idx.data_ptr(), self.val.data_ptr(),
@@ -109,12 +122,15 @@ class DeltaPipeline:
         self.apply(stream)
 
     # -- host read-back (tests) --------------------------------------------
-    def delta(self):
-        """(idx, val) on the host, sorted by idx; and the cursor value."""
+    def delta(self, raw=False):
+        """(idx, val) on the host, sorted by idx (as written with raw=True);
+        and the cursor value."""
         total = int(self.cursor.item())
         k = min(total, self.capacity)
         idx = self.idx[:k].cpu().numpy()
         val = self.val[:k].cpu().numpy().view("uint16")
+        if raw:
+            return idx, val, total
         order = idx.argsort(kind="stable")
         return idx[order], val[order], total
 

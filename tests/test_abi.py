@@ -189,3 +189,27 @@ def test_plan_rejects_duplicate_source_for_one_rank():
     dup.dst_base = numel[dup.rank]
     numel[dup.rank] += size
     assert _create_status(spec, ops=ops + [dup], numel=numel) == B.DTE_ERR_PLAN
+
+
+def test_ordered_workspace_and_argument_errors():
+    assert B.dte_ordered_workspace_bytes(-1) == -1
+    assert B.dte_ordered_workspace_bytes(1 << 41) == -1
+    small = B.dte_ordered_workspace_bytes(0)
+    big = B.dte_ordered_workspace_bytes(1_000_000)
+    assert small > 0 and small % 256 == 0
+    assert big >= small + 10 * 1_000_000
+    hp = B.dte_adamw_step(1e-6, 0.9, 0.999, 1e-8, 0.01, 100)
+    ext = lambda *a: B.raw_status("dte_extract_delta_ordered", *a)  # noqa: E731
+    need = B.dte_ordered_workspace_bytes(4)
+    # zero-length input: legal, nothing enqueued
+    assert ext(None, None, None, 0, 0, ctypes.byref(hp), None, None, 0, None, None, 0, None,
+               None) == B.DTE_OK
+    # missing, too small or misaligned workspace
+    assert ext(16, 16, 16, 4, 0, ctypes.byref(hp), 16, 16, 4, 16, None, need, None,
+               None) == B.DTE_ERR_ARG
+    assert ext(16, 16, 16, 4, 0, ctypes.byref(hp), 16, 16, 4, 16, 256, need - 1, None,
+               None) == B.DTE_ERR_ARG
+    assert ext(16, 16, 16, 4, 0, ctypes.byref(hp), 16, 16, 4, 16, 16, need, None,
+               None) == B.DTE_ERR_ARG
+    assert ext(16, 16, 16, -1, 0, ctypes.byref(hp), 16, 16, 4, 16, 256, need, None,
+               None) == B.DTE_ERR_ARG

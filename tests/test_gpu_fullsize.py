@@ -141,6 +141,24 @@ def test_qwen3_8b_tp4_full(qwen3_8b):
     check_theta_hat_windows(wl, p, m, v, spec, pick_windows(wl, 1))
 
 
+def test_qwen3_8b_ordered_full(qwen3_8b):
+    """Ordered extract at full size: the raw output is the oracle's sorted
+    delta, entry for entry."""
+    wl, res, p, m, v = qwen3_8b
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=int(wl.numel * 0.02), ordered=True)
+    pipe.reset()
+    pipe.extract(p, m, v, wl.hp)
+    sync()
+    idx, val, total = pipe.delta(raw=True)
+    assert total == res.idx.size
+    assert np.array_equal(idx, res.idx)
+    assert np.array_equal(val, res.val)
+    pipe.close()
+    del pipe
+    torch.cuda.empty_cache()
+
+
 def test_qwen3_8b_tp8_apply_full(qwen3_8b):
     """The Qwen3-8B delta remapped to eight TP=8 receivers and applied."""
     wl, res, p, m, v = qwen3_8b

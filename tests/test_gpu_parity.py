@@ -329,3 +329,68 @@ def test_values_at_bf16_rounding_midpoints(lr):
     assert total == want_idx.size
     assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val)
     pipe.close()
+
+
+@pytest.mark.parametrize("make", [
+    lambda: W.scaled_dense(layers=2, tp=2, lr=1e-6),
+    lambda: W.scaled_dense(layers=2, tp=2, lr=1e-4),
+    lambda: W.tiny_block(),
+])
+def test_ordered_extract_is_ascending_and_exact(make):
+    """dte_extract_delta_ordered writes exactly the oracle's sorted delta,
+    identical bytes on repeated calls, ascending across appended calls."""
+    wl = make()
+    say("case: ordered extract", wl.name, wl.hp.lr)
+    res, st = oracle_state(wl)
+    p, m, v = dev(st["p"]), dev(st["m"]), dev(st["v"])
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=max(1, res.idx.size), ordered=True)
+    for _ in range(2):
+        pipe.reset()
+        pipe.extract(p, m, v, wl.hp)
+        sync()
+        idx, val, total = pipe.delta(raw=True)
+        assert total == res.idx.size
+        assert np.array_equal(idx, res.idx) and np.array_equal(val, res.val)
+    # two appended sub-ranges, the second misaligned and ragged
+    cut = (wl.numel // 3) | 1
+    pipe.reset()
+    pipe.extract(p[:cut], m[:cut], v[:cut], wl.hp, n=cut, index_base=0)
+    pipe.extract(p[cut:], m[cut:], v[cut:], wl.hp, n=wl.numel - cut, index_base=cut)
+    sync()
+    idx, val, total = pipe.delta(raw=True)
+    assert total == res.idx.size
+    assert np.array_equal(idx, res.idx) and np.array_equal(val, res.val)
+    # theta_hat in ordered mode
+    prev = torch.empty_like(p)
+    pipe.reset()
+    pipe.extract(p, m, v, wl.hp, out_prev=prev)
+    sync()
+    assert np.array_equal(prev.cpu().numpy().view(np.uint32), st["ph"].view(np.uint32))
+    idx, val, _ = pipe.delta(raw=True)
+    assert np.array_equal(idx, res.idx) and np.array_equal(val, res.val)
+    # the ordered delta through remap and apply
+    pl = oplan.build_plan(wl)
+    pipe.remap()
+    sync()
+    buckets, counts = pipe.buckets()
+    want = oremap.remap(pl, res.idx, res.val)
+    for r in range(pl.nranks):
+        assert counts[r] == want[r][0].size
+        assert np.array_equal(buckets[r][0], want[r][0])
+        assert np.array_equal(buckets[r][1], want[r][1])
+    pipe.close()
+
+
+def test_ordered_extract_capacity_overflow_reports_total():
+    wl = W.scaled_dense(layers=1, tp=2, lr=1e-4)
+    say("case: ordered extract overflow", wl.name)
+    res, st = oracle_state(wl)
+    p, m, v = dev(st["p"]), dev(st["m"]), dev(st["v"])
+    cap = res.idx.size // 3
+    pipe = DeltaPipeline(layouts.build_spec(wl), capacity=cap, ordered=True)
+    pipe.reset()
+    pipe.extract(p, m, v, wl.hp)
+    sync()
+    assert int(pipe.cursor.item()) == res.idx.size
+    pipe.close()

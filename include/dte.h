@@ -40,6 +40,10 @@ typedef int32_t dte_status;
 #define DTE_ERR_PLAN 2     /* transfer plan failed validation */
 #define DTE_ERR_CAPACITY 3 /* reserved: output capacity exceeded (reported via counters) */
 #define DTE_ERR_HIP 4      /* a HIP runtime call failed */
+#define DTE_ERR_IO 5       /* a file could not be read or written (dte_store.h) */
+#define DTE_ERR_CORRUPT 6  /* stored data failed its checksum or format check */
+#define DTE_ERR_CHAIN 7    /* a stored version does not extend the local base version */
+#define DTE_ERR_UNSUPPORTED 8 /* the requested codec is not available on this host */
 
 #define DTE_MAX_DIMS 4     /* tensor rank limit of segments and plan operations */
 #define DTE_MAX_RANKS 64   /* receiver ranks per plan */

@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdte.so")
-SOURCES = ["dte_api.hip", "extract.hip", "remap.hip"]
+SOURCES = ["dte_api.hip", "extract.hip", "remap.hip", "store.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

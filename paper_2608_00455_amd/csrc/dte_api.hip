@@ -266,6 +266,10 @@ const char* dte_status_string(dte_status status)
     case DTE_ERR_PLAN: return "DTE_ERR_PLAN: transfer plan failed validation";
     case DTE_ERR_CAPACITY: return "DTE_ERR_CAPACITY: output capacity exceeded";
     case DTE_ERR_HIP: return "DTE_ERR_HIP: HIP runtime error";
+    case DTE_ERR_IO: return "DTE_ERR_IO: file read or write failed";
+    case DTE_ERR_CORRUPT: return "DTE_ERR_CORRUPT: stored data failed its checksum or format check";
+    case DTE_ERR_CHAIN: return "DTE_ERR_CHAIN: version does not extend the local base version";
+    case DTE_ERR_UNSUPPORTED: return "DTE_ERR_UNSUPPORTED: codec not available";
     default: return "unknown dte_status";
     }
 }

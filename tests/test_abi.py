@@ -15,17 +15,22 @@ from paper_2608_00455_amd import binding as B
 from paper_2608_00455_amd import layouts
 from synth import workloads as W
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "dte.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include")
 
 
 def declared():
-    text = open(HEADER).read()
-    return sorted(set(re.findall(r"^[A-Za-z_][\w \t\*]*?\b(dte_\w+)\s*\(", text, re.M)))
+    names = set()
+    for h in sorted(os.listdir(INCLUDE)):
+        if h.endswith(".h"):
+            text = open(os.path.join(INCLUDE, h)).read()
+            names |= set(re.findall(r"^[A-Za-z_][\w \t\*]*?\b(dte_\w+)\s*\(", text, re.M))
+    return sorted(names)
 
 
 def test_every_declared_symbol_is_exported():
+    from paper_2608_00455_amd import store
     names = declared()
-    assert set(names) == set(B.EXPORTED)
+    assert set(names) == set(B.EXPORTED) | set(store.EXPORTED)
     lib = ctypes.CDLL(B.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n

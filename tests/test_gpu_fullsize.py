@@ -159,6 +159,40 @@ def test_qwen3_8b_ordered_full(qwen3_8b):
     torch.cuda.empty_cache()
 
 
+def test_qwen3_8b_store_round_trip_full(qwen3_8b, tmp_path):
+    """The full Qwen3-8B delta published from the device (ordered extract,
+    zstd chunks) and read back into device memory equals the oracle's."""
+    import time
+    from paper_2608_00455_amd import store as S
+    wl, res, p, m, v = qwen3_8b
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=int(wl.numel * 0.02), ordered=True)
+    pipe.reset()
+    pipe.extract(p, m, v, wl.hp)
+    segs = S.segments_of([t.name for t in wl.tensors], wl.flat_begins(),
+                         [t.numel for t in wl.tensors])
+    opt = S.Options(threads=16)
+    t0 = time.perf_counter()
+    st = S.write_part_device(tmp_path, 1, 0, segs, pipe.idx.data_ptr(), pipe.val.data_ptr(),
+                             pipe.cursor.data_ptr(), pipe.capacity, opt)
+    assert S.commit(tmp_path, 1, 0, 1)
+    t1 = time.perf_counter()
+    pipe.idx.fill_(-1)
+    n, _ = S.read_device(tmp_path, 1, 0, pipe.idx.data_ptr(), pipe.val.data_ptr(), pipe.capacity,
+                         threads=16)
+    t2 = time.perf_counter()
+    say("fullsize: store %d entries, %d chunks, %.1f MB raw, %.1f MB stored, publish %.2f s, "
+        "read %.2f s" % (st.entries, st.chunks, st.raw_bytes / 1e6, st.stored_bytes / 1e6,
+                         t1 - t0, t2 - t1))
+    assert n == res.idx.size == st.entries
+    pipe.cursor.fill_(n)
+    idx, val, _ = pipe.delta(raw=True)
+    assert np.array_equal(idx, res.idx) and np.array_equal(val, res.val)
+    pipe.close()
+    del pipe
+    torch.cuda.empty_cache()
+
+
 def test_qwen3_8b_tp8_apply_full(qwen3_8b):
     """The Qwen3-8B delta remapped to eight TP=8 receivers and applied."""
     wl, res, p, m, v = qwen3_8b

@@ -117,6 +117,43 @@ def measured_traffic(workload_name, kernel):
     return rec["traffic_bytes_per_launch"]
 
 
+def storage_leg(root, wl, spec, p, m, v, hp, cap):
+    """Publish one ordered delta through the storage path (writer part +
+    commit: device narrowing, pinned staging, zstd level 3 on 16 host
+    threads, files, manifest) and read it back into device memory; host
+    wall-clock times, not part of the step."""
+    import shutil
+
+    import torch
+
+    from paper_2608_00455_amd import store as S
+    from paper_2608_00455_amd.pipeline import DeltaPipeline
+
+    d = os.path.join(root, "dte_store_bench")
+    shutil.rmtree(d, ignore_errors=True)
+    pipe = DeltaPipeline(spec, capacity=cap, ordered=True)
+    pipe.reset()
+    pipe.extract(p, m, v, hp)
+    torch.cuda.synchronize()
+    segs = S.segments_of([t.name for t in wl.tensors], wl.flat_begins(),
+                         [t.numel for t in wl.tensors])
+    opt = S.Options(threads=16)
+    t0 = time.perf_counter()
+    st = S.write_part_device(d, 1, 0, segs, pipe.idx.data_ptr(), pipe.val.data_ptr(),
+                             pipe.cursor.data_ptr(), pipe.capacity, opt)
+    S.commit(d, 1, 0, 1)
+    t1 = time.perf_counter()
+    n, _ = S.read_device(d, 1, 0, pipe.idx.data_ptr(), pipe.val.data_ptr(), pipe.capacity,
+                         threads=16)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    pipe.close()
+    shutil.rmtree(d, ignore_errors=True)
+    return {"entries": int(n), "chunks": st.chunks, "raw_bytes": st.raw_bytes,
+            "stored_bytes": st.stored_bytes, "ratio": st.raw_bytes / max(1, st.stored_bytes),
+            "publish_s": t1 - t0, "read_s": t2 - t1, "codec": "zstd-3", "threads": 16}
+
+
 def copy_calibration(gib):
     """A plain copy of known size: reads and writes gib GiB once per launch."""
     import torch
@@ -155,6 +192,14 @@ def main():
                          "0.25 for the learning-rate sweep)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--settle", type=float, default=15.0, metavar="SECONDS",
+                    help="wait before allocating the state: device memory that a process "
+                         "released moments earlier is handed out in less contiguous pieces "
+                         "until the driver has reclaimed it, which slows streaming kernels")
+    ap.add_argument("--store", default=None, metavar="DIR",
+                    help="also publish the step's delta through the storage path (ordered "
+                         "extract, zstd chunks under DIR) and read it back to the device; "
+                         "reports the times and sizes under 'storage'")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only time a plain device copy of GIB GiB (for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -177,6 +222,9 @@ def main():
     if args.norm_group:
         wl = W.with_norm_group(wl)
     hp = wl.hp if args.lr is None else type(wl.hp)(lr=args.lr)
+    if args.settle > 0:
+        log("bench: settling %.0f s before allocating" % args.settle)
+        time.sleep(args.settle)
     spec = layouts.build_spec(wl)
     n = spec.total                           # elements of the trainer shard
     log("bench: workload %s, %d elements, lr %g" % (wl.name, n, hp.lr))
@@ -273,7 +321,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
-        "config": {"workload": wl.name, "elements": n, "changed": changed, "extract_calls": len(runs),
+        "config": {"workload": wl.name, "elements": n, "changed": changed, "extract_calls": len(runs), "settle_s": args.settle,
                    "ordered": bool(args.ordered),
                    "change_fraction": c, "receiver_ranks": len(counts),
                    "routed_entries": routed, "lr": hp.lr,
@@ -287,6 +335,8 @@ def main():
     }
     if not apply_only:
         out["config"].update({"extract_ms": ext_ms, "remap_ms": rem_ms, "apply_ms": app_ms})
+    if args.store and not apply_only:
+        out["storage"] = storage_leg(args.store, wl, spec, p, m, v, hp, cap)
     del p, m, v
     pipe.close()
     torch.cuda.empty_cache()

@@ -18,7 +18,8 @@ _lib = None
 class Scalars(ctypes.Structure):
     _fields_ = [("lrb1", ctypes.c_float), ("rbc2", ctypes.c_float), ("eps", ctypes.c_float),
                 ("decay", ctypes.c_float), ("b1", ctypes.c_float), ("b2", ctypes.c_float),
-                ("omb1", ctypes.c_float), ("omb2", ctypes.c_float)]
+                ("omb1", ctypes.c_float), ("omb2", ctypes.c_float), ("lr", ctypes.c_float),
+                ("bc1", ctypes.c_float), ("bc2", ctypes.c_float), ("order", ctypes.c_int32)]
 
     def bits(self):
         """The four scalars of the inverse as binary32 bit patterns."""
@@ -35,8 +36,8 @@ def lib():
         L = ctypes.CDLL(_LIB_PATH)
         P = ctypes.c_void_p
         L.oracle_derive_scalars.restype = ctypes.c_int
-        L.oracle_derive_scalars.argtypes = [ctypes.c_double] * 5 + [ctypes.c_int64,
-                                                                    ctypes.POINTER(Scalars)]
+        L.oracle_derive_scalars.argtypes = [ctypes.c_double] * 5 + [
+            ctypes.c_int64, ctypes.c_int32, ctypes.POINTER(Scalars)]
         L.oracle_adamw_forward.restype = None
         L.oracle_adamw_forward.argtypes = [P, P, P, P, ctypes.c_int64, ctypes.POINTER(Scalars),
                                            P, P, P]
@@ -53,10 +54,11 @@ def lib():
 
 
 def derive_scalars(hp) -> Scalars:
-    """Step scalars of the inverse and the forward step (sec. 3.1; appendix A)."""
+    """Step scalars of the inverse and the forward step (sec. 3.1; appendix A),
+    for the operation order hp.order (0 folded, 1 literal eq. adamw_inverse)."""
     s = Scalars()
     rc = lib().oracle_derive_scalars(hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay,
-                                     hp.step, ctypes.byref(s))
+                                     hp.step, getattr(hp, "order", 0), ctypes.byref(s))
     if rc != 0:
         raise ValueError("invalid AdamW hyperparameters: %r" % (hp,))
     return s

@@ -22,6 +22,12 @@
  *     inverse (sec. 3.1, eq. adamw_inverse):              ph = (p + u) / DECAY
  * which is the paper's expression with the bias corrections folded into
  * the two scalars, evaluated left to right.
+ *
+ * Literal order (order = 1): eq. adamw_inverse operation by operation, with
+ * LR = lr, BC1 = 1 - beta1^t, BC2 = 1 - beta2^t rounded once to binary32:
+ *     u  = LR * ((m / BC1) / (sqrt(v / BC2) + EPS))
+ * (four divisions with the one by DECAY), used by the forward step and the
+ * inverse alike.
  */
 #include <math.h>
 #include <stdint.h>
@@ -30,14 +36,17 @@
 typedef struct {
     float lrb1, rbc2, eps, decay;   /* inverse and forward */
     float b1, b2, omb1, omb2;       /* forward moment update only */
+    float lr, bc1, bc2;             /* literal order */
+    int32_t order;                  /* 0: folded, 1: literal */
 } oracle_scalars;
 
 /* Step scalars (sec. 3.1, eq. adamw_inverse; appendix A): binary64 math,
  * one rounding to binary32 each.  Returns 0, or -1 on invalid input. */
 int oracle_derive_scalars(double lr, double beta1, double beta2, double eps, double wd,
-                          int64_t step, oracle_scalars* out)
+                          int64_t step, int32_t order, oracle_scalars* out)
 {
-    if (step < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
+    if (step < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) ||
+        (order != 0 && order != 1))
         return -1;
     const double bc1 = 1.0 - pow(beta1, (double)step);
     const double bc2 = 1.0 - pow(beta2, (double)step);
@@ -51,12 +60,25 @@ int oracle_derive_scalars(double lr, double beta1, double beta2, double eps, dou
     out->b2 = (float)beta2;
     out->omb1 = (float)(1.0 - beta1);
     out->omb2 = (float)(1.0 - beta2);
+    out->lr = (float)lr;
+    out->bc1 = (float)bc1;
+    out->bc2 = (float)bc2;
+    out->order = order;
     return 0;
 }
 
-/* Adaptive step term u = (LRB1*m) / (sqrt(v*RBC2) + EPS), one element. */
+/* Adaptive step term u = (LRB1*m) / (sqrt(v*RBC2) + EPS), one element
+ * (literal order: LR * ((m / BC1) / (sqrt(v / BC2) + EPS))). */
 static float oracle_step_term(float m, float v, const oracle_scalars* s)
 {
+    if (s->order == 1) {
+        const float mh = m / s->bc1;   /* m_t / (1 - beta1^t)         */
+        const float vq = v / s->bc2;   /* v_t / (1 - beta2^t)         */
+        const float sq = sqrtf(vq);
+        const float d = sq + s->eps;
+        const float r = mh / d;
+        return s->lr * r;              /* eta_t times the ratio       */
+    }
     const float vh = v * s->rbc2;      /* v / (1 - beta2^t)           */
     const float sq = sqrtf(vh);        /* sqrt of the corrected moment */
     const float den = sq + s->eps;     /* + epsilon                    */

@@ -51,15 +51,22 @@ class Tensor:
         return n
 
 
+ORDER_FOLDED, ORDER_LITERAL = 0, 1
+
+
 @dataclass(frozen=True)
 class StepHP:
-    """Hyperparameters of the one AdamW step (one parameter group)."""
+    """Hyperparameters of the one AdamW step (one parameter group), and the
+    binary32 operation order of the step and its inverse (ORDER_FOLDED:
+    bias corrections folded into two scalars; ORDER_LITERAL: the inverse's
+    printed expression with its four divisions)."""
     lr: float
     beta1: float = 0.9
     beta2: float = 0.999
     eps: float = 1e-8
     weight_decay: float = 0.01
     step: int = 100
+    order: int = ORDER_FOLDED
 
 
 @dataclass(frozen=True)

@@ -205,3 +205,85 @@ def test_c_build_rounds_every_operation():
     got = core.invert(p, m, v, sc)
     want = _bruteforce_inverse(p, m, v, sc)
     assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+# -- literal operation order (eq. adamw_inverse as printed) -----------------
+
+LIT = W.ORDER_LITERAL
+
+
+@pytest.mark.parametrize("lr", [0.0, 1e-6, 1e-4])
+@pytest.mark.parametrize("step", [1, 100, 10000])
+def test_literal_scalars_are_exact_values_rounded_once(lr, step):
+    hp = W.StepHP(lr=lr, step=step, order=LIT)
+    sc = core.derive_scalars(hp)
+    assert sc.order == 1
+    b1, b2 = Fraction(hp.beta1), Fraction(hp.beta2)
+    want = {"lr": Fraction(lr), "bc1": 1 - b1 ** step, "bc2": 1 - b2 ** step}
+    for name, x in want.items():
+        assert f32_bits(getattr(sc, name)) == f32_bits(f32(float(x))), name
+
+
+def _bruteforce_literal(p, m, v, s):
+    out = []
+    for pi, mi, vi in zip(p.tolist(), m.tolist(), v.tolist()):
+        mh = f32(mi / s.bc1)
+        vq = f32(vi / s.bc2)
+        d = f32(f32(math.sqrt(vq)) + s.eps)
+        u = f32(s.lr * f32(mh / d))
+        out.append(f32(f32(pi + u) / s.decay))
+    return np.array(out, np.float32)
+
+
+def test_c_build_literal_rounds_every_operation():
+    rng = np.random.default_rng(8)
+    n = 20000
+    sc = core.derive_scalars(W.StepHP(lr=1e-4, order=LIT))
+    p = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    m = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+    v = np.abs(rng.standard_normal(n) * 1e-6).astype(np.float32)
+    p[:8] = np.array([1e-45, -1e-45, 1e-39, -3e-39, 0.0, -0.0, 3e38, -3e38], np.float32)
+    m[8:16] = np.array([1e-45, -1e-40, 0.0, 1e-20, -1e-30, 2e-38, 1.0, -1.0], np.float32)
+    v[16:24] = np.array([0.0, 1e-45, 1e-40, 1e-38, 1e-30, 1.0, 100.0, 1e-20], np.float32)
+    got = core.invert(p, m, v, sc)
+    want = _bruteforce_literal(p, m, v, sc)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+@pytest.mark.parametrize("lr", [1e-6, 1e-4, 1e-2])
+def test_literal_inverse_within_bound_of_exact(lr):
+    """The literal order against exact eq. adamw_inverse: u carries at most
+    about 9 roundings (LR, BC1, m/BC1, BC2, v/BC2, sqrt, + EPS, the ratio,
+    the product); then the same half-ulps as the folded order."""
+    hp = W.StepHP(lr=lr, order=LIT)
+    sc = core.derive_scalars(hp)
+    n = 3000
+    p_prev, m_prev, v_prev, g = _state(n, seed=12)
+    p, m, v = core.adamw_forward(p_prev, m_prev, v_prev, g, sc)
+    ph = core.invert(p, m, v, sc)
+    ex = _exact_scalars(hp)
+    ex["lr"] = Fraction(hp.lr)
+    ex["lrb1_den"] = 1 - Fraction(hp.beta1) ** hp.step
+    for i in range(n):
+        want = _exact_inverse(float(p[i]), float(m[i]), float(v[i]), ex)
+        err = abs(Fraction(float(ph[i])) - want)
+        ulp = Fraction(float(np.spacing(np.float32(abs(float(want))))))
+        u = abs(want * ex["decay"] - Fraction(float(p[i])))
+        bound = 2 * ulp + 10 * u * Fraction(1, 1 << 24) / ex["decay"]
+        assert err <= bound, (i, float(ph[i]), float(want))
+
+
+@pytest.mark.parametrize("lr", [1e-6, 1e-4])
+def test_literal_round_trip_and_difference_from_folded(lr):
+    n = 1 << 16
+    p_prev, m_prev, v_prev, g = _state(n, seed=22)
+    lit = core.derive_scalars(W.StepHP(lr=lr, order=LIT))
+    fol = core.derive_scalars(W.StepHP(lr=lr))
+    p, m, v = core.adamw_forward(p_prev, m_prev, v_prev, g, lit)
+    ph = core.invert(p, m, v, lit)
+    scale = np.maximum(np.abs(p_prev), np.abs(p - p_prev))
+    assert np.all(np.abs(ph - p_prev) <= 2 * np.spacing(scale))
+    # the two orders round differently somewhere, and stay within 2 ulp
+    pf, _, _ = core.adamw_forward(p_prev, m_prev, v_prev, g, fol)
+    assert np.count_nonzero(pf != p) > 0
+    assert np.all(np.abs(pf - p) <= 2 * np.spacing(np.maximum(np.abs(p), np.abs(p - p_prev))))

@@ -183,6 +183,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen3_8b_tp4")
     ap.add_argument("--lr", type=float, default=None)
+    ap.add_argument("--literal", action="store_true",
+                    help="literal operation order of the AdamW inverse (four divisions)")
     ap.add_argument("--ordered", action="store_true",
                     help="dte_extract_delta_ordered (ascending, deterministic delta)")
     ap.add_argument("--norm-group", action="store_true",
@@ -222,6 +224,9 @@ def main():
     if args.norm_group:
         wl = W.with_norm_group(wl)
     hp = wl.hp if args.lr is None else type(wl.hp)(lr=args.lr)
+    if args.literal:
+        hp = type(hp)(lr=hp.lr, beta1=hp.beta1, beta2=hp.beta2, eps=hp.eps,
+                      weight_decay=hp.weight_decay, step=hp.step, order=W.ORDER_LITERAL)
     if args.settle > 0:
         log("bench: settling %.0f s before allocating" % args.settle)
         time.sleep(args.settle)
@@ -322,7 +327,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
         "config": {"workload": wl.name, "elements": n, "changed": changed, "extract_calls": len(runs), "settle_s": args.settle,
-                   "ordered": bool(args.ordered),
+                   "ordered": bool(args.ordered), "order": "literal" if args.literal else "folded",
                    "change_fraction": c, "receiver_ranks": len(counts),
                    "routed_entries": routed, "lr": hp.lr,
                    "step_algorithmic_bytes": step_bytes,

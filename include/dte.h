@@ -48,11 +48,17 @@ typedef int32_t dte_status;
 #define DTE_MAX_DIMS 4     /* tensor rank limit of segments and plan operations */
 #define DTE_MAX_RANKS 64   /* receiver ranks per plan */
 
+#define DTE_ORDER_FOLDED 0   /* bias corrections folded into two scalars */
+#define DTE_ORDER_LITERAL 1  /* eq. adamw_inverse as printed: four divisions */
+
 /* Hyperparameters of one AdamW step of one parameter group (paper sec. 3.1,
  * eq. adamw_moments and eq. adamw_inverse; appendix A): learning rate eta_t,
  * moment coefficients beta1, beta2, epsilon, the group's decoupled weight
- * decay lambda, and the step index t of the step just taken (t >= 1).
- * Valid: lr >= 0 finite, 0 <= beta < 1, eps >= 0 finite, 1 - lr*wd > 0. */
+ * decay lambda, and the step index t of the step just taken (t >= 1);
+ * `order` selects the binary32 operation order of the step and its inverse
+ * (DTE_ORDER_FOLDED or DTE_ORDER_LITERAL, see dte_scalars); `reserved` must
+ * be 0.  Valid: lr >= 0 finite, 0 <= beta < 1, eps >= 0 finite,
+ * 1 - lr*wd > 0. */
 typedef struct {
     double lr;
     double beta1;
@@ -60,25 +66,35 @@ typedef struct {
     double eps;
     double weight_decay;
     int64_t step;
+    int32_t order;
+    int32_t reserved;
 } dte_adamw_step;
 
 /* The step scalars of the inverse, each computed in binary64 from
  * dte_adamw_step and rounded once to binary32:
  *   lrb1  = lr / (1 - beta1^t)      rbc2  = 1 / (1 - beta2^t)
  *   eps   = eps                     decay = 1 - lr * weight_decay
+ *   lr    = lr                      bc1 = 1 - beta1^t,  bc2 = 1 - beta2^t
  * With them the inverse of sec. 3.1, eq. adamw_inverse, is evaluated per
  * element, left to right, as
- *   u = (lrb1 * m) / (sqrt(v * rbc2) + eps);   theta_hat = (theta + u) / decay
- * (the paper's expression with the bias corrections folded into the two
- * scalars, as a fused optimizer folds them). */
+ *   folded:  u = (lrb1 * m) / (sqrt(v * rbc2) + eps)
+ *   literal: u = lr * ((m / bc1) / (sqrt(v / bc2) + eps))
+ *   theta_hat = (theta + u) / decay
+ * (folded: the bias corrections folded into two scalars, as a fused
+ * optimizer folds them; literal: the printed expression, four divisions).
+ * dte_adamw_forward uses the same u. */
 typedef struct {
     float lrb1;
     float rbc2;
     float eps;
     float decay;
+    float lr;
+    float bc1;
+    float bc2;
+    int32_t order;
 } dte_scalars;
 
-/* Host-only.  Derive the four scalars above.  Errors: DTE_ERR_ARG for a null
+/* Host-only.  Derive the scalars above.  Errors: DTE_ERR_ARG for a null
  * pointer or an invalid dte_adamw_step. */
 dte_status dte_derive_scalars(const dte_adamw_step* hp, dte_scalars* out);
 
@@ -87,7 +103,8 @@ dte_status dte_derive_scalars(const dte_adamw_step* hp, dte_scalars* out);
  * canonical_delta_detection).
  *
  * For each element i in [0, n):
- *   theta_hat = inverse(p[i], m[i], v[i])            (sec. 3.1, see dte_scalars)
+ *   theta_hat = inverse(p[i], m[i], v[i])            (sec. 3.1, see dte_scalars;
+ *                                                     in hp->order)
  *   b_old = BF16(theta_hat), b_new = BF16(p[i])     (round to nearest even on
  *           the binary32 pattern; overflow to +-inf; any NaN -> 0x7FC0)
  *   changed if b_old != b_new as 16-bit patterns     (+0 and -0 differ)
@@ -251,7 +268,7 @@ dte_status dte_apply(const dte_plan* plan, uint16_t* const* shards, const int64_
  * device buffers p, m, v (theta, m, v of step t-1 in, of step t out) with
  * gradient g, n elements each, in the same binary32 operation order:
  *   m = beta1*m + (1-beta1)*g;  v = beta2*v + (1-beta2)*(g*g);
- *   u = (lrb1*m) / (sqrt(v*rbc2) + eps);  p = decay*p - u
+ *   u as in dte_scalars for hp->order;  p = decay*p - u
  * (beta1, beta2, 1-beta1, 1-beta2 rounded once to binary32).  Provided so
  * a trainer (or a test) can produce states whose inverse is exact up to the
  * rounding of p.  Errors: DTE_ERR_ARG, DTE_ERR_HIP. */

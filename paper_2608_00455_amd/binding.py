@@ -27,15 +27,20 @@ class DteError(RuntimeError):
         self.status = status
 
 
+DTE_ORDER_FOLDED, DTE_ORDER_LITERAL = 0, 1
+
+
 class dte_adamw_step(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double),
                 ("beta2", ctypes.c_double), ("eps", ctypes.c_double),
-                ("weight_decay", ctypes.c_double), ("step", ctypes.c_int64)]
+                ("weight_decay", ctypes.c_double), ("step", ctypes.c_int64),
+                ("order", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class dte_scalars(ctypes.Structure):
     _fields_ = [("lrb1", ctypes.c_float), ("rbc2", ctypes.c_float), ("eps", ctypes.c_float),
-                ("decay", ctypes.c_float)]
+                ("decay", ctypes.c_float), ("lr", ctypes.c_float), ("bc1", ctypes.c_float),
+                ("bc2", ctypes.c_float), ("order", ctypes.c_int32)]
 
 
 class dte_segment(ctypes.Structure):
@@ -105,7 +110,8 @@ def _check(fn, st):
 def _hp(hp) -> dte_adamw_step:
     if isinstance(hp, dte_adamw_step):
         return hp
-    return dte_adamw_step(hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay, hp.step)
+    return dte_adamw_step(hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay, hp.step,
+                          getattr(hp, "order", DTE_ORDER_FOLDED), 0)
 
 
 def _ptrs(xs):

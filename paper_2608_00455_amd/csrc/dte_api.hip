@@ -57,6 +57,8 @@ bool valid_hp(const dte_adamw_step* hp)
     if (!std::isfinite(hp->weight_decay)) return false;
     if (hp->step < 1) return false;
     if (!(1.0 - hp->lr * hp->weight_decay > 0.0)) return false;
+    if (hp->order != DTE_ORDER_FOLDED && hp->order != DTE_ORDER_LITERAL) return false;
+    if (hp->reserved != 0) return false;
     return true;
 }
 
@@ -75,6 +77,10 @@ AllScalars derive(const dte_adamw_step& hp)
     a.s.rbc2 = (float)(1.0 / bc2);
     a.s.eps = (float)hp.eps;
     a.s.decay = (float)(1.0 - hp.lr * hp.weight_decay);
+    a.s.lr = (float)hp.lr;
+    a.s.bc1 = (float)bc1;
+    a.s.bc2 = (float)bc2;
+    a.s.order = hp.order;
     a.b1 = (float)hp.beta1;
     a.b2 = (float)hp.beta2;
     a.omb1 = (float)(1.0 - hp.beta1);
@@ -318,6 +324,16 @@ dte::ExtractParams extract_params(const float* p, const float* m, const float* v
         a.rd_lo = std::nextafter(r, 0.0f);
         a.rd_hi = std::nextafter(r, INFINITY);
     }
+    a.literal = sc.s.order == DTE_ORDER_LITERAL;
+    a.lr = sc.s.lr;
+    a.bc1 = sc.s.bc1;
+    a.bc2 = sc.s.bc2;
+    // literal order: the "unchanged" proof holds only for these scalars
+    // (extract.hip, proven_unchanged)
+    a.lit_filter = a.eps >= 0x1p-40f && a.lr <= 0x1p20f && a.bc1 >= 0x1p-20f && a.bc2 >= 0x1p-20f;
+    a.floor = a.lit_filter
+                  ? std::nextafter((float)(0x1p-124 / std::min(1.0, (double)a.eps)), INFINITY)
+                  : 0x1p-126f;
     a.out_idx = out_idx;
     a.out_val = out_val;
     a.capacity = capacity;
@@ -443,6 +459,10 @@ dte_status dte_adamw_forward(float* p, float* m, float* v, const float* g, int64
     a.b2 = sc.b2;
     a.omb1 = sc.omb1;
     a.omb2 = sc.omb2;
+    a.literal = sc.s.order == DTE_ORDER_LITERAL;
+    a.lr = sc.s.lr;
+    a.bc1 = sc.s.bc1;
+    a.bc2 = sc.s.bc2;
     return dte::launch_adamw_forward(a, current_cus(), (hipStream_t)stream) == hipSuccess
                ? DTE_OK
                : DTE_ERR_HIP;

@@ -21,6 +21,7 @@ struct OrderRun {
     int32_t wave;         // global wave number (launch order)
 };
 
+// Operation order of the step and its inverse (dte_scalars).
 struct ExtractParams {
     const float* p;
     const float* m;
@@ -29,6 +30,10 @@ struct ExtractParams {
     int64_t index_base;   // flat trainer offset of element 0
     float lrb1, rbc2, eps, decay;
     float rd_lo, rd_hi;   // binary32 bracket of 1/decay: rd_lo <= 1/decay <= rd_hi
+    int32_t literal;      // order: 0 folded, 1 literal
+    float lr, bc1, bc2;   // literal order
+    int32_t lit_filter;   // literal order: the "unchanged" proof may be used
+    float floor;          // literal order: additive term of the proof's bound
     int64_t* out_idx;
     uint16_t* out_val;
     int64_t capacity;
@@ -81,6 +86,8 @@ struct ForwardParams {
     const float* g;
     int64_t n;
     float lrb1, rbc2, eps, decay, b1, b2, omb1, omb2;
+    float lr, bc1, bc2;
+    int32_t literal;
 };
 
 hipError_t launch_adamw_forward(const ForwardParams& a, int cus, hipStream_t stream);

@@ -69,6 +69,19 @@ __device__ __forceinline__ float step_term(float m, float v, float lrb1, float r
     return num / den;
 }
 
+// The same term in the literal order of eq. adamw_inverse:
+// lr * ((m / bc1) / (sqrt(v / bc2) + eps)), six binary32 operations.
+__device__ __forceinline__ float step_term_literal(float m, float v, float lr, float bc1, float bc2,
+                                                   float eps)
+{
+    const float mh = m / bc1;
+    const float vq = v / bc2;
+    const float sq = __builtin_sqrtf(vq);
+    const float d = sq + eps;
+    const float r = mh / d;
+    return lr * r;
+}
+
 // BF16 pattern of x: round to nearest even on the binary32 pattern; any NaN
 // gives 0x7FC0.  (For non-NaN x the 32-bit sum cannot wrap.)
 __device__ __forceinline__ uint32_t bf16_bits(float x)
@@ -105,33 +118,49 @@ __device__ __forceinline__ f32x4 load4(const float* base, int64_t e, int64_t n)
 // overflowing intermediates make B non-finite or too large, never too small,
 // except a reciprocal flushed to zero, covered by the floor 2^-126 (a |u|
 // below it cannot move a |p| >= 2^-100, and a smaller |p| fails the test).
-template <bool kDecayOne>
+//
+// Literal order: the same B bounds the literal u when every intermediate of
+// both evaluations is a normal number (each then carries one rounding of
+// relative error, about ten in all, far inside 2^-16).  The host allows the
+// proof only when eps >= 2^-40, lr <= 2^20 and both bias corrections are
+// >= 2^-20.  Then d = sqrt(v/bc2) + eps >= 2^-40, so a subnormal v/bc2
+// moves d by at most 2^-75 (relative 2^-35); subnormal m/bc1, lrb1*m or
+// m/bc1/d move u by at most 2^-125/eps in all, the floor (`floor`, set by
+// the host) used instead of 2^-126; |m| <= 2^64 keeps m/bc1 and m/bc1/d
+// finite (other elements take the exact path); v*rbc2 is clamped to the
+// largest finite value so that it cannot overflow where v/bc2 does not
+// (a NaN stays NaN).
+template <bool kDecayOne, bool kLit>
 __device__ __forceinline__ bool proven_unchanged(float p, float m, float v, const ExtractParams& a)
 {
     const float num = a.lrb1 * m;
-    const float vh = v * a.rbc2;
+    float vh = v * a.rbc2;
+    if (kLit) vh = vh > 0x1.fffffep127f ? 0x1.fffffep127f : vh;
+    const bool in_range = !kLit || (__float_as_uint(m) & 0x7FFFFFFFu) <= 0x5F800000u;
     const float den = __builtin_amdgcn_sqrtf(vh) + a.eps;
     const float q = __builtin_fabsf(num) * __builtin_amdgcn_rcpf(den);
-    const float b = __builtin_fmaf(q, 1.0000153f, 0x1p-126f);   // NaN stays NaN
+    const float b = __builtin_fmaf(q, 1.0000153f, kLit ? a.floor : 0x1p-126f);   // NaN stays NaN
     const float hi = p + __builtin_copysignf(b, m);
     const uint32_t up = __float_as_uint(p), uh = __float_as_uint(hi);
     const uint32_t rp = up + 0x7FFFu + ((up >> 16) & 1u);
     const uint32_t rh = uh + 0x7FFFu + ((uh >> 16) & 1u);
-    if (kDecayOne) return (rp ^ rh) < 0x10000u;
+    if (kDecayOne) return in_range & ((rp ^ rh) < 0x10000u);
     const float x0 = p * a.rd_lo, x1 = p * a.rd_hi, x2 = hi * a.rd_lo, x3 = hi * a.rd_hi;
     const float mn = __builtin_fminf(__builtin_fminf(x0, x1), __builtin_fminf(x2, x3));
     const float mx = __builtin_fmaxf(__builtin_fmaxf(x0, x1), __builtin_fmaxf(x2, x3));
     const uint32_t un = __float_as_uint(mn), ux = __float_as_uint(mx);
     const uint32_t rn = un + 0x7FFFu + ((un >> 16) & 1u);
     const uint32_t rx = ux + 0x7FFFu + ((ux >> 16) & 1u);
-    return (rp ^ rn) < 0x10000u && (rp ^ rx) < 0x10000u && (mn == mn) && (mx == mx) && (hi == hi);
+    return in_range & ((rp ^ rn) < 0x10000u) & ((rp ^ rx) < 0x10000u) & (mn == mn) & (mx == mx) &
+           (hi == hi);
 }
 
 // Exact inverse and change test of one element (sec. 3.1 / 3.2.1).
-template <bool kDecayOne>
+template <bool kDecayOne, bool kLit>
 __device__ __forceinline__ float exact_prev(float p, float m, float v, const ExtractParams& a)
 {
-    const float u = step_term(m, v, a.lrb1, a.rbc2, a.eps);
+    const float u = kLit ? step_term_literal(m, v, a.lr, a.bc1, a.bc2, a.eps)
+                         : step_term(m, v, a.lrb1, a.rbc2, a.eps);
     const float num = p + u;
     return kDecayOne ? num : num / a.decay;
 }
@@ -252,7 +281,7 @@ __device__ __forceinline__ void stage_changed(const ExtractParams& a, const Wave
 
 // Exact inverse of every queued candidate, 64 per pass; changed ones are
 // staged.  Empties the queue.
-template <bool kDecayOne>
+template <bool kDecayOne, bool kLit>
 __device__ void drain_queue(const ExtractParams& a, const WaveStage& st, int& queued, Staging& so,
                             int lane)
 {
@@ -264,7 +293,7 @@ __device__ void drain_queue(const ExtractParams& a, const WaveStage& st, int& qu
         uint16_t bn = 0;
         if (i < queued) {
             const float p = st.qp[i];
-            const float ph = exact_prev<kDecayOne>(p, st.qm[i], st.qv[i], a);
+            const float ph = exact_prev<kDecayOne, kLit>(p, st.qm[i], st.qv[i], a);
             bn = (uint16_t)bf16_bits(p);
             changed = bf16_bits(ph) != bn;
             key = st.qkey[i];
@@ -300,7 +329,7 @@ __device__ __forceinline__ void load_tile(const ExtractParams& a, int64_t t0, in
     }
 }
 
-template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev>
+template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev, bool kLit>
 __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0, int lane,
                                              Staging& so, int& queued, const WaveStage& st,
                                              uint32_t iter, const f32x4* P, const f32x4* M,
@@ -319,7 +348,7 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const float p = P[j][c];
-                const float ph = exact_prev<kDecayOne>(p, M[j][c], V[j][c], a);
+                const float ph = exact_prev<kDecayOne, kLit>(p, M[j][c], V[j][c], a);
                 prev[c] = ph;
                 bn[c] = bf16_bits(p);
                 sel[c] = (kFull || off + c < rem) && bf16_bits(ph) != bn[c];
@@ -351,10 +380,12 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
 #pragma unroll
             for (int c = 0; c < 4; ++c)
                 sel[c] = (kFull || off + c < rem) &&
-                         !proven_unchanged<kDecayOne>(P[j][c], M[j][c], V[j][c], a);
+                         ((kLit && !a.lit_filter) ||
+                          !proven_unchanged<kDecayOne, kLit>(P[j][c], M[j][c], V[j][c], a));
             const Slot4 r = select4(sel);
             if (r.count != 0) {
-                if (queued + r.count > kQueue) drain_queue<kDecayOne>(a, st, queued, so, lane);
+                if (queued + r.count > kQueue)
+                    drain_queue<kDecayOne, kLit>(a, st, queued, so, lane);
                 const int base = queued + lanes_before(r);
                 int k = 0;
 #pragma unroll
@@ -374,7 +405,7 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
 }
 
 // Wave tiles [first, last) of the range; kFull: each lies inside [0, n).
-template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev>
+template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev, bool kLit>
 __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_t first,
                                                          int64_t last)
 {
@@ -401,10 +432,10 @@ __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_
     for (int64_t t = w_first; t < w_last; ++t) {
         f32x4 P[kVec], M[kVec], V[kVec];
         load_tile<kFull, kVecLoads>(a, t * kWaveTile, lane, P, M, V);
-        process_tile<kFull, kVecLoads, kDecayOne, kWritePrev>(a, t * kWaveTile, lane, so,
+        process_tile<kFull, kVecLoads, kDecayOne, kWritePrev, kLit>(a, t * kWaveTile, lane, so,
                                                              queued, st, iter++, P, M, V);
     }
-    if (queued > 0) drain_queue<kDecayOne>(a, st, queued, so, lane);
+    if (queued > 0) drain_queue<kDecayOne, kLit>(a, st, queued, so, lane);
     if (so.staged > 0) flush_wave(a, st, so, lane);
     if (a.runs && lane == 0) a.wave_count[st.wave] = so.flushed;
 }
@@ -428,7 +459,8 @@ __global__ __launch_bounds__(256) void adamw_forward_kernel(ForwardParams a)
             const float v1 = a.b2 * V[c];
             const float v2 = a.omb2 * g2;
             const float vt = v1 + v2;
-            const float u = step_term(mt, vt, a.lrb1, a.rbc2, a.eps);
+            const float u = a.literal ? step_term_literal(mt, vt, a.lr, a.bc1, a.bc2, a.eps)
+                                      : step_term(mt, vt, a.lrb1, a.rbc2, a.eps);
             const float dp = a.decay * P[c];
             P[c] = dp - u;
             M[c] = mt;
@@ -454,7 +486,7 @@ __global__ __launch_bounds__(256) void adamw_forward_kernel(ForwardParams a)
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Launch over wave tiles [first, last); returns the number of waves.
-template <bool F, bool V, bool D>
+template <bool F, bool V, bool D, bool L>
 int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_grid,
                      int32_t wave0, hipStream_t s)
 {
@@ -463,24 +495,24 @@ int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_g
     const dim3 grid((unsigned)(blocks < max_grid ? blocks : max_grid));
     a.wave0 = wave0;
     if (a.out_prev)
-        hipLaunchKernelGGL((extract_kernel<F, V, D, true>), grid, dim3(kBlock), 0, s, a, first,
+        hipLaunchKernelGGL((extract_kernel<F, V, D, true, L>), grid, dim3(kBlock), 0, s, a, first,
                            last);
     else
-        hipLaunchKernelGGL((extract_kernel<F, V, D, false>), grid, dim3(kBlock), 0, s, a, first,
+        hipLaunchKernelGGL((extract_kernel<F, V, D, false, L>), grid, dim3(kBlock), 0, s, a, first,
                            last);
     return (int32_t)grid.x * kWaves;
 }
 
-template <bool D>
+template <bool D, bool L>
 int32_t launch_all(const ExtractParams& a, bool vec, int64_t max_grid, hipStream_t s)
 {
     const int64_t full = a.n / kWaveTile;
     const int64_t ntiles = (a.n + kWaveTile - 1) / kWaveTile;
     if (vec) {
-        const int32_t w = launch_tiles<true, true, D>(a, 0, full, max_grid, 0, s);  // unguarded
-        return w + launch_tiles<false, true, D>(a, full, ntiles, max_grid, w, s);   // ragged tail
+        const int32_t w = launch_tiles<true, true, D, L>(a, 0, full, max_grid, 0, s);  // unguarded
+        return w + launch_tiles<false, true, D, L>(a, full, ntiles, max_grid, w, s);   // ragged tail
     }
-    return launch_tiles<false, false, D>(a, 0, ntiles, max_grid, 0, s);           // scalar loads
+    return launch_tiles<false, false, D, L>(a, 0, ntiles, max_grid, 0, s);           // scalar loads
 }
 
 // ---- ordered mode: runs to ascending positions ----------------------------
@@ -559,8 +591,13 @@ hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream, i
     if (a.runs && max_grid > kMaxOrderedWaves / kWaves - 1) max_grid = kMaxOrderedWaves / kWaves - 1;
     const bool vec = aligned16(a.p) && aligned16(a.m) && aligned16(a.v) &&
                      (a.out_prev == nullptr || aligned16(a.out_prev));
-    const int32_t w = (a.decay == 1.0f) ? launch_all<true>(a, vec, max_grid, stream)
-                                        : launch_all<false>(a, vec, max_grid, stream);
+    int32_t w;
+    if (a.literal)
+        w = (a.decay == 1.0f) ? launch_all<true, true>(a, vec, max_grid, stream)
+                              : launch_all<false, true>(a, vec, max_grid, stream);
+    else
+        w = (a.decay == 1.0f) ? launch_all<true, false>(a, vec, max_grid, stream)
+                              : launch_all<false, false>(a, vec, max_grid, stream);
     if (waves) *waves = w;
     return hipGetLastError();
 }

@@ -39,19 +39,21 @@ def test_every_declared_symbol_is_exported():
 @pytest.mark.parametrize("lr", [0.0, 1e-7, 1e-6, 1e-5, 1e-4, 3e-3])
 @pytest.mark.parametrize("step", [1, 7, 100, 5000])
 @pytest.mark.parametrize("wd", [0.0, 0.01, 0.1])
-def test_scalars_bit_equal_oracle(lr, step, wd):
-    hp = W.StepHP(lr=lr, step=step, weight_decay=wd)
+@pytest.mark.parametrize("order", [W.ORDER_FOLDED, W.ORDER_LITERAL])
+def test_scalars_bit_equal_oracle(lr, step, wd, order):
+    hp = W.StepHP(lr=lr, step=step, weight_decay=wd, order=order)
     got = B.dte_derive_scalars(hp)
     want = ocore.derive_scalars(hp)
-    for f in ("lrb1", "rbc2", "eps", "decay"):
+    for f in ("lrb1", "rbc2", "eps", "decay", "lr", "bc1", "bc2"):
         a = ctypes.c_float(getattr(got, f))
         b = ctypes.c_float(getattr(want, f))
         assert bytes(a) == bytes(b), f
+    assert got.order == want.order == order
 
 
 @pytest.mark.parametrize("bad", [
     dict(step=0), dict(beta1=1.0), dict(beta2=-0.1), dict(lr=-1e-6), dict(lr=float("nan")),
-    dict(lr=100.0, weight_decay=0.01), dict(eps=float("inf")),
+    dict(lr=100.0, weight_decay=0.01), dict(eps=float("inf")), dict(order=2), dict(reserved=1),
 ])
 def test_invalid_hyperparameters(bad):
     hp = B.dte_adamw_step(1e-6, 0.9, 0.999, 1e-8, 0.01, 100)

@@ -285,3 +285,23 @@ def test_qwen3_8b_layers_mcore_full(rank):
     pipe.close()
     del pipe, p, m, v
     torch.cuda.empty_cache()
+
+
+def test_qwen3_8b_layers_literal_order_full():
+    """Four Qwen3-8B layers at lr 1e-4 (DECAY != 1, 14 % changed) with the
+    literal operation order of eq. adamw_inverse, forward step included."""
+    wl = W.qwen3_8b_layers_sweep(1e-4)
+    hp = W.StepHP(lr=1e-4, order=W.ORDER_LITERAL)
+    say("fullsize: literal order")
+    res = orun.extract(wl, hp=hp)
+    p, m, v = generate_state(wl, hp)
+    spec = layouts.build_spec(wl)
+    pl = oplan.build_plan(wl)
+    pipe = DeltaPipeline(spec, capacity=int(wl.numel * 0.25), shards=sentinel_shards(spec))
+    pipe.step(p, m, v, hp)
+    sync()
+    check_delta(pipe, res)
+    check_buckets_and_shards(pipe, pl, oremap.remap(pl, res.idx, res.val))
+    pipe.close()
+    del pipe, p, m, v
+    torch.cuda.empty_cache()

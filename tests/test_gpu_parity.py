@@ -123,17 +123,24 @@ def test_full_path_tiny_block_generated_state(tiny):
     pipe.close()
 
 
+@pytest.mark.parametrize("order", [W.ORDER_FOLDED, W.ORDER_LITERAL])
 @pytest.mark.parametrize("lr", [0.0, 1e-7, 1e-6, 1e-5, 1e-4, 1e-2])
-def test_learning_rates_small_dense(lr):
+def test_learning_rates_small_dense(lr, order):
     wl = W.scaled_dense(layers=2, tp=2, lr=lr)
-    say("case: lr sweep", wl.name, lr)
-    res, st = oracle_state(wl)
+    hp = W.StepHP(lr=lr, order=order)
+    say("case: lr sweep", wl.name, lr, order)
+    res, st = oracle_state(wl, hp)
     spec = layouts.build_spec(wl)
     pipe = DeltaPipeline(spec, capacity=wl.numel)
+    # the device forward step in the same order gives the same state
+    gp, gm, gv = generate_state(wl, hp)
+    for name, t in (("p", gp), ("m", gm), ("v", gv)):
+        assert np.array_equal(t.cpu().numpy().view(np.uint32), st[name].view(np.uint32)), name
+    del gp, gm, gv
     p, m, v = dev(st["p"]), dev(st["m"]), dev(st["v"])
     prev = torch.empty_like(p)
     pipe.reset()
-    pipe.extract(p, m, v, wl.hp, out_prev=prev)
+    pipe.extract(p, m, v, hp, out_prev=prev)
     pipe.remap()
     sync()
     assert_delta_equal(pipe, res)
@@ -145,6 +152,11 @@ def test_learning_rates_small_dense(lr):
         assert np.array_equal(buckets[r][1], want[r][1])
     if lr == 0.0:
         assert res.idx.size == 0
+    # the filtered path (no theta_hat requested) finds the same delta
+    pipe.reset()
+    pipe.extract(p, m, v, hp)
+    sync()
+    assert_delta_equal(pipe, res)
     pipe.close()
 
 
@@ -182,8 +194,9 @@ def test_ragged_misaligned_and_appended_ranges():
     pipe.close()
 
 
-def test_special_values():
-    say("case: special values")
+@pytest.mark.parametrize("order", [W.ORDER_FOLDED, W.ORDER_LITERAL])
+def test_special_values(order):
+    say("case: special values", order)
     rng = np.random.default_rng(3)
     n = 5000
     p = (rng.standard_normal(n) * 0.02).astype(np.float32)
@@ -200,7 +213,7 @@ def test_special_values():
                              0x80000001, 0x7F800001, 0xFFC00000, 0x007F8000, 0x3FFF8000],
                             np.uint32).view(np.float32)
     for lr in (1e-6, 1e-4, 3e-1):
-        hp = W.StepHP(lr=lr)
+        hp = W.StepHP(lr=lr, order=order)
         sc = ocore.derive_scalars(hp)
         want_idx, want_val, want_ph = ocore.detect(p, m, v, sc, 1000)
         spec = layouts.build_spec(W.scaled_dense(layers=1, tp=2))
@@ -215,6 +228,12 @@ def test_special_values():
         nan = np.isnan(want_ph)
         assert np.array_equal(np.isnan(got_ph), nan)
         assert np.array_equal(got_ph.view(np.uint32)[~nan], want_ph.view(np.uint32)[~nan])
+        # and through the "unchanged" proof (no theta_hat requested)
+        pipe.reset()
+        pipe.extract(dev(p), dev(m), dev(v), hp, index_base=1000)
+        sync()
+        idx, val, total = pipe.delta()
+        assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val), lr
         pipe.close()
 
 
@@ -298,7 +317,8 @@ def test_empty_delta_leaves_shards_untouched():
 
 
 @pytest.mark.parametrize("lr", [1e-7, 1e-6, 1e-4, 3e-2])
-def test_values_at_bf16_rounding_midpoints(lr):
+@pytest.mark.parametrize("order", [W.ORDER_FOLDED, W.ORDER_LITERAL])
+def test_values_at_bf16_rounding_midpoints(lr, order):
     """Weights a few binary32 ulps from BF16 rounding midpoints (where the
     reconstruction decides the pattern), zeros, subnormals and both signs of
     the moment: every element parity-checked against the oracle."""
@@ -317,7 +337,7 @@ def test_values_at_bf16_rounding_midpoints(lr):
     m[1::7] = -0.0
     v = np.abs(rng.standard_normal(n) * 10.0 ** rng.uniform(-12, -4, n)).astype(np.float32)
     v[::5] = 0.0
-    hp = W.StepHP(lr=lr)
+    hp = W.StepHP(lr=lr, order=order)
     want_idx, want_val, _ = ocore.detect(p, m, v, ocore.derive_scalars(hp), 0)
     assert want_idx.size > 100
     spec = layouts.build_spec(W.scaled_dense(layers=1, tp=2))
@@ -394,3 +414,46 @@ def test_ordered_extract_capacity_overflow_reports_total():
     sync()
     assert int(pipe.cursor.item()) == res.idx.size
     pipe.close()
+
+
+@pytest.mark.parametrize("eps", [1e-8, 1e-13])
+def test_literal_order_at_the_proof_guards(eps):
+    """Literal order around every bound that decides whether the
+    "unchanged" proof may be used (|m| near 2^-100 and 2^64, v near 2^-126
+    and 2^100, lrb1 * m near the subnormal range, eps below 2^-40 disabling
+    the proof), with weights from tiny to huge: bit-exact delta."""
+    say("case: literal guards", eps)
+    rng = np.random.default_rng(17)
+    mags_m = np.float32([0.0, 2.0 ** -101, 2.0 ** -100, 2.0 ** -99, 2.0 ** -60, 2.0 ** -30,
+                         1e-4, 1.0, 2.0 ** 63, 2.0 ** 64, 2.0 ** 65, 3e38])
+    mags_v = np.float32([0.0, 2.0 ** -149, 2.0 ** -127, 2.0 ** -126, 2.0 ** -125, 1e-12, 1e-6,
+                         1.0, 2.0 ** 99, 2.0 ** 100, 2.0 ** 101, 3e38])
+    mags_p = np.float32([0.0, 1e-40, 2.0 ** -100, 1e-30, 1e-10, 0.02, 1.0, 1e20, 2.0 ** 100,
+                         1e36, 3e38])
+    grid = np.array(np.meshgrid(mags_p, mags_m, mags_v, indexing="ij")).reshape(3, -1)
+    k = grid.shape[1]
+    reps = 24
+    p = np.tile(grid[0], reps).astype(np.float32)
+    m = np.tile(grid[1], reps).astype(np.float32)
+    v = np.tile(grid[2], reps).astype(np.float32)
+    # random signs and a few-ulp jitter so some weights sit near BF16 midpoints
+    p *= rng.choice(np.float32([-1, 1]), p.size)
+    m *= rng.choice(np.float32([-1, 1]), m.size)
+    jit = rng.integers(-3, 4, p.size).astype(np.int64)
+    pb = p.view(np.uint32).astype(np.int64)
+    mid = (pb & ~0xFFFF) | 0x8000
+    pb = np.where(np.arange(p.size) % 2 == 0, mid + jit, pb) & 0xFFFFFFFF
+    p = pb.astype(np.uint32).view(np.float32)
+    assert p.size == k * reps
+    for lr in (1e-7, 1e-4, 0.5):
+        hp = W.StepHP(lr=lr, eps=eps, order=W.ORDER_LITERAL)
+        want_idx, want_val, _ = ocore.detect(p, m, v, ocore.derive_scalars(hp), 0)
+        pipe = DeltaPipeline(layouts.build_spec(W.scaled_dense(layers=1, tp=2)),
+                             capacity=p.size)
+        pipe.reset()
+        pipe.extract(dev(p), dev(m), dev(v), hp)
+        sync()
+        idx, val, total = pipe.delta()
+        assert total == want_idx.size, lr
+        assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val), lr
+        pipe.close()

@@ -24,7 +24,8 @@
  * before LATEST, so a reader never sees a partial version.
  *
  * Chunk file: a 40-byte header (magic "DTEC", format 1, segment, index
- * transform, first entry, count, payload bytes), then the payload (count
+ * transform, first entry (ordinal among the writer's entries of the
+ * segment), count, payload bytes), then the payload (count
  * uint32 segment-local indices, ascending, stored as gaps with transform 1
  * or as values with transform 0, then count uint16 BF16 patterns), either
  * verbatim (codec none) or as one Zstandard frame (codec zstd).  The
@@ -54,6 +55,27 @@ typedef struct {
     int64_t flat_begin;
     int64_t numel;
 } dte_store_segment;
+
+/* A contiguous range [sender_begin, sender_end) of the writer's flat shard
+ * that holds whole rows of a box of canonical segment `segment` (the
+ * converter's map for a trainer layout such as Megatron-Core, sec. 3.2.1
+ * and appendix B): shard element sender_begin + q, with q = row *
+ * local_cols + col, is element (canon_row0 + row, canon_col0 + col) of the
+ * segment viewed as rows of canon_cols, i.e. its canonical local index is
+ * (canon_row0 + row) * canon_cols + canon_col0 + col.  segment = -1: the
+ * range's entries are published by another writer (replicated tensors).
+ * Pieces are sorted by sender_begin and disjoint; the pieces a writer
+ * publishes for one segment cover ascending, disjoint canonical ranges. */
+typedef struct {
+    int64_t sender_begin;
+    int64_t sender_end;
+    int32_t segment;
+    int32_t reserved;
+    int64_t local_cols;
+    int64_t canon_cols;
+    int64_t canon_row0;
+    int64_t canon_col0;
+} dte_store_piece;
 
 typedef struct {
     int32_t codec;           /* 0: none, 1: zstd (needs libzstd.so.1 at run time) */
@@ -99,7 +121,9 @@ dte_status dte_store_write_part_device(const char* dir, int64_t version, int32_t
  * for the first): *committed = 1 and manifest.json then LATEST written.  If
  * the parts hold no entry at all, nothing is published (*committed = 0,
  * the version directory is removed, LATEST unchanged).  A missing part is
- * DTE_ERR_IO with nothing published. */
+ * DTE_ERR_IO with nothing published.  Several writers may publish entries
+ * of one segment (tensor-parallel trainer ranks); their entries must be
+ * disjoint, which the writers' piece tables guarantee. */
 dte_status dte_store_commit(const char* dir, int64_t version, int64_t parent, int32_t nwriters,
                             int32_t* committed);
 
@@ -115,8 +139,10 @@ dte_status dte_store_chain(const char* dir, int64_t base, int64_t latest, int64_
 /* Entries of committed version `version`, whose parent must equal `base`
  * (the version the destination applied last; else DTE_ERR_CHAIN): every
  * chunk is checked against its manifest length and XXH64 and its own
- * header before use (DTE_ERR_CORRUPT).  Output: ascending flat offsets
- * (segment flat_begin from the manifest + local index) and values;
+ * header before use (DTE_ERR_CORRUPT).  Output: flat offsets (segment
+ * flat_begin from the manifest + local index) and values, grouped by
+ * segment, then writer, ascending within each (segment, writer) group
+ * (ascending overall when every segment has a single writer);
  * *count = the version's entry total; entries beyond capacity are not
  * written (then call again with capacity >= *count). */
 dte_status dte_store_read_host(const char* dir, int64_t version, int64_t base, int64_t* idx,
@@ -130,6 +156,23 @@ dte_status dte_store_read_host(const char* dir, int64_t version, int64_t base, i
 dte_status dte_store_read_device(const char* dir, int64_t version, int64_t base, int64_t* idx,
                                  uint16_t* val, int64_t capacity, int64_t* count,
                                  int32_t threads, dte_store_stats* stats, void* stream);
+
+/* As dte_store_write_part_host / _device for a writer whose shard is not
+ * laid out as the canonical segments: idx are offsets in the writer's flat
+ * shard, mapped to canonical segments by `pieces` (npiece entries). */
+dte_status dte_store_write_part_host_mapped(const char* dir, int64_t version, int32_t writer,
+                                            const dte_store_segment* segs, int32_t nseg,
+                                            const dte_store_piece* pieces, int32_t npiece,
+                                            const int64_t* idx, const uint16_t* val, int64_t count,
+                                            const dte_store_options* opt, dte_store_stats* stats);
+
+dte_status dte_store_write_part_device_mapped(const char* dir, int64_t version, int32_t writer,
+                                              const dte_store_segment* segs, int32_t nseg,
+                                              const dte_store_piece* pieces, int32_t npiece,
+                                              const int64_t* idx, const uint16_t* val,
+                                              const int64_t* count, int64_t capacity,
+                                              const dte_store_options* opt, dte_store_stats* stats,
+                                              void* stream);
 
 /* XXH64 of n bytes with the given seed (the chunk checksum). */
 uint64_t dte_store_xxh64(const void* data, int64_t n, uint64_t seed);

@@ -662,16 +662,31 @@ __global__ void ascending_kernel(const int64_t* idx, int64_t n, int32_t* bad)
     if (!ok) atomicOr(bad, 1);
 }
 
-// local[e] = idx[e] - begin[s] for the segment s holding entry e (entries
-// already checked to lie inside segments).
-__global__ void narrow_kernel(const int64_t* idx, int64_t n, const int64_t* begin, int32_t nseg,
-                              uint32_t* local)
+// A contiguous range [begin, end) of the writer's flat shard holding whole
+// rows of a box of canonical segment `segment` (see dte_store_piece).
+struct Piece {
+    int64_t begin, end;
+    int32_t segment;          // -1: not published by this writer
+    int64_t local_cols, canon_cols, row0, col0;
+};
+
+__host__ __device__ inline int64_t canon_local(const Piece& pc, int64_t q)
+{
+    if (pc.local_cols == pc.canon_cols && pc.col0 == 0) return pc.row0 * pc.canon_cols + q;
+    const int64_t row = q / pc.local_cols;
+    return (pc.row0 + row) * pc.canon_cols + pc.col0 + (q - row * pc.local_cols);
+}
+
+// local[e]: canonical segment-local index of entry e, from the piece holding
+// it (entries already checked to lie inside pieces; pieces sorted by begin).
+__global__ void narrow_kernel(const int64_t* idx, int64_t n, const int64_t* begin,
+                              const Piece* pieces, int32_t npiece, uint32_t* local)
 {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
         const int64_t x = idx[e];
-        const int64_t s = lower_bound_i64(begin, nseg, x + 1) - 1;   // last begin <= x
-        local[e] = s >= 0 ? (uint32_t)(x - begin[s]) : 0u;
+        const int64_t k = lower_bound_i64(begin, npiece, x + 1) - 1;   // last begin <= x
+        local[e] = k >= 0 ? (uint32_t)canon_local(pieces[k], x - pieces[k].begin) : 0u;
     }
 }
 
@@ -718,22 +733,78 @@ std::vector<Segment> to_segments(const dte_store_segment* segs, int32_t nseg)
 }
 
 // One chunk to encode: entries [lo, lo + count) of the writer's delta, all
-// in segment `segment`, `first` entries of the segment before it.
+// in piece `piece` of canonical segment `segment`, `first` entries of this
+// writer in the segment before it.
 struct ChunkJob {
     int32_t segment;
+    int32_t piece;
     int64_t lo;
     int64_t first;
     int64_t count;
 };
 
-std::vector<ChunkJob> plan_chunks(const std::vector<int64_t>& lo, const std::vector<int64_t>& hi,
-                                  int64_t chunk_entries)
+std::vector<ChunkJob> plan_chunks(const std::vector<Piece>& pcs, const std::vector<int64_t>& lo,
+                                  const std::vector<int64_t>& hi, int64_t chunk_entries)
 {
     std::vector<ChunkJob> jobs;
-    for (size_t s = 0; s < lo.size(); ++s)
-        for (int64_t a = lo[s]; a < hi[s]; a += chunk_entries)
-            jobs.push_back({(int32_t)s, a, a - lo[s], std::min(chunk_entries, hi[s] - a)});
+    std::map<int32_t, int64_t> ordinal;
+    for (size_t k = 0; k < pcs.size(); ++k) {
+        if (pcs[k].segment < 0) continue;
+        int64_t& first = ordinal[pcs[k].segment];
+        for (int64_t a = lo[k]; a < hi[k]; a += chunk_entries) {
+            const int64_t c = std::min(chunk_entries, hi[k] - a);
+            jobs.push_back({pcs[k].segment, (int32_t)k, a, first, c});
+            first += c;
+        }
+    }
     return jobs;
+}
+
+// Pieces sorted and disjoint in the shard; each owned piece a whole-row box
+// inside its segment; the owned pieces of one segment in ascending, disjoint
+// canonical order (so each writer's entries of a segment ascend).
+bool valid_pieces(const std::vector<Piece>& pcs, const std::vector<Segment>& segs)
+{
+    int64_t end = INT64_MIN;
+    std::map<int32_t, int64_t> last;   // per segment: largest canonical index so far
+    for (const Piece& pc : pcs) {
+        if (pc.begin < end || pc.end < pc.begin || pc.begin < 0) return false;
+        end = pc.end;
+        if (pc.segment < 0) continue;
+        if ((size_t)pc.segment >= segs.size() || pc.local_cols <= 0 || pc.canon_cols <= 0 ||
+            pc.row0 < 0 || pc.col0 < 0 || pc.col0 + pc.local_cols > pc.canon_cols ||
+            (pc.end - pc.begin) % pc.local_cols != 0)
+            return false;
+        const int64_t rows = (pc.end - pc.begin) / pc.local_cols;
+        if (rows == 0) continue;
+        const int64_t numel = segs[pc.segment].numel;
+        if (pc.canon_cols > numel || pc.row0 + rows > numel / pc.canon_cols ||
+            numel % pc.canon_cols != 0)
+            return false;
+        const int64_t lo = canon_local(pc, 0), hi = canon_local(pc, pc.end - pc.begin - 1);
+        auto it = last.find(pc.segment);
+        if (it != last.end() && lo <= it->second) return false;
+        last[pc.segment] = hi;
+    }
+    return true;
+}
+
+std::vector<Piece> identity_pieces(const std::vector<Segment>& segs)
+{
+    std::vector<Piece> pcs;
+    for (size_t i = 0; i < segs.size(); ++i)
+        pcs.push_back({segs[i].begin, segs[i].begin + segs[i].numel, (int32_t)i, segs[i].numel,
+                       segs[i].numel, 0, 0});
+    return pcs;
+}
+
+std::vector<Piece> to_pieces(const dte_store_piece* p, int32_t n)
+{
+    std::vector<Piece> pcs((size_t)n);
+    for (int32_t i = 0; i < n; ++i)
+        pcs[i] = {p[i].sender_begin, p[i].sender_end, p[i].segment, p[i].local_cols, p[i].canon_cols,
+                  p[i].canon_row0, p[i].canon_col0};
+    return pcs;
 }
 
 dte_status write_part_file(const std::string& dir, int64_t version, int32_t writer,
@@ -832,14 +903,16 @@ dte_status load_manifest(const std::string& dir, int64_t version, Manifest& m)
         if (c.segment < 0 || (size_t)c.segment >= m.segs.size() || c.count <= 0 ||
             c.count > ((int64_t)1 << 26) || c.raw_bytes != 6 * c.count || c.bytes < 40)
             return DTE_ERR_CORRUPT;
-        if (i > 0) {   // ascending segments; within one, consecutive entry ranges
+        // ascending (segment, writer); within one, consecutive entry ranges from 0
+        const bool same = i > 0 && m.chunks[i - 1].segment == c.segment &&
+                          m.chunks[i - 1].writer == c.writer;
+        if (i > 0) {
             const ChunkMeta& p = m.chunks[i - 1];
-            if (c.segment < p.segment || (c.segment == p.segment && c.first != p.first + p.count))
+            if (c.segment < p.segment || (c.segment == p.segment && c.writer < p.writer))
                 return DTE_ERR_CORRUPT;
-            if (c.segment != p.segment && c.first != 0) return DTE_ERR_CORRUPT;
-        } else if (c.first != 0) {
-            return DTE_ERR_CORRUPT;
         }
+        if (c.first != (same ? m.chunks[i - 1].first + m.chunks[i - 1].count : 0))
+            return DTE_ERR_CORRUPT;
         m.offset.push_back(pos);
         pos += c.count;
     }
@@ -905,41 +978,45 @@ uint64_t dte_store_xxh64(const void* data, int64_t n, uint64_t seed)
     return xxh64(data, (size_t)n, seed);
 }
 
-dte_status dte_store_write_part_host(const char* dir, int64_t version, int32_t writer,
-                                     const dte_store_segment* segs, int32_t nseg,
-                                     const int64_t* idx, const uint16_t* val, int64_t count,
-                                     const dte_store_options* opt, dte_store_stats* stats)
+}  // extern "C"
+
+namespace {
+
+dte_status write_host_impl(const char* dir, int64_t version, int32_t writer,
+                           const std::vector<Segment>& sg, const std::vector<Piece>& pcs,
+                           const int64_t* idx, const uint16_t* val, int64_t count,
+                           const dte_store_options* opt, dte_store_stats* stats)
 {
-    if (!common_write_args(dir, version, writer, segs, nseg, opt) || count < 0 ||
-        (count > 0 && (!idx || !val)))
-        return DTE_ERR_ARG;
+    if (count < 0 || (count > 0 && (!idx || !val)) || !valid_pieces(pcs, sg)) return DTE_ERR_ARG;
     if (opt->codec == 1 && !zstd().ok) return DTE_ERR_UNSUPPORTED;
-    const std::vector<Segment> sg = to_segments(segs, nseg);
-    // entries strictly ascending and inside segments
-    std::vector<int64_t> lo(sg.size()), hi(sg.size());
-    int64_t inside = 0;
+    // entries strictly ascending and inside pieces
     for (int64_t e = 1; e < count; ++e)
         if (idx[e] <= idx[e - 1]) return DTE_ERR_ARG;
-    for (size_t s = 0; s < sg.size(); ++s) {
-        lo[s] = std::lower_bound(idx, idx + count, sg[s].begin) - idx;
-        hi[s] = std::lower_bound(idx, idx + count, sg[s].begin + sg[s].numel) - idx;
-        inside += hi[s] - lo[s];
+    std::vector<int64_t> lo(pcs.size()), hi(pcs.size());
+    int64_t inside = 0;
+    for (size_t k = 0; k < pcs.size(); ++k) {
+        lo[k] = std::lower_bound(idx, idx + count, pcs[k].begin) - idx;
+        hi[k] = std::lower_bound(idx, idx + count, pcs[k].end) - idx;
+        inside += hi[k] - lo[k];
     }
     if (inside != count) return DTE_ERR_ARG;
     const std::string d(dir);
     if (!make_dir(d) || !make_dir(vdir(d, version))) return DTE_ERR_IO;
-    const std::vector<ChunkJob> jobs = plan_chunks(lo, hi, opt->chunk_entries);
+    const std::vector<ChunkJob> jobs = plan_chunks(pcs, lo, hi, opt->chunk_entries);
     std::vector<ChunkMeta> metas;
     std::mutex mm;
     FirstError err;
+    int64_t published = 0;
+    for (const ChunkJob& j : jobs) published += j.count;
     {
         Pool pool(opt->threads);
         for (size_t k = 0; k < jobs.size(); ++k) {
             pool.push([&, k] {
                 const ChunkJob& j = jobs[k];
+                const Piece& pc = pcs[j.piece];
                 std::vector<uint32_t> local((size_t)j.count);
                 for (int64_t i = 0; i < j.count; ++i)
-                    local[i] = (uint32_t)(idx[j.lo + i] - sg[j.segment].begin);
+                    local[i] = (uint32_t)canon_local(pc, idx[j.lo + i] - pc.begin);
                 encode_and_write(vdir(d, version), writer, (int64_t)k, j, local.data(), val + j.lo, *opt,
                                  mm, metas, err);
             });
@@ -947,18 +1024,16 @@ dte_status dte_store_write_part_host(const char* dir, int64_t version, int32_t w
     }
     if (err.get() != DTE_OK) return err.get();
     fill_stats(stats, metas);
-    return write_part_file(d, version, writer, sg, *opt, metas, count);
+    return write_part_file(d, version, writer, sg, *opt, metas, published);
 }
 
-dte_status dte_store_write_part_device(const char* dir, int64_t version, int32_t writer,
-                                       const dte_store_segment* segs, int32_t nseg,
-                                       const int64_t* idx, const uint16_t* val,
-                                       const int64_t* count, int64_t capacity,
-                                       const dte_store_options* opt, dte_store_stats* stats,
-                                       void* stream)
+dte_status write_device_impl(const char* dir, int64_t version, int32_t writer,
+                             const std::vector<Segment>& sg, const std::vector<Piece>& pcs,
+                             const int64_t* idx, const uint16_t* val, const int64_t* count,
+                             int64_t capacity, const dte_store_options* opt, dte_store_stats* stats,
+                             void* stream)
 {
-    if (!common_write_args(dir, version, writer, segs, nseg, opt) || !count || capacity < 0)
-        return DTE_ERR_ARG;
+    if (!count || capacity < 0 || !valid_pieces(pcs, sg)) return DTE_ERR_ARG;
     if (opt->codec == 1 && !zstd().ok) return DTE_ERR_UNSUPPORTED;
     const hipStream_t s = (hipStream_t)stream;
     int64_t n = 0;
@@ -966,47 +1041,50 @@ dte_status dte_store_write_part_device(const char* dir, int64_t version, int32_t
         hipStreamSynchronize(s) != hipSuccess)
         return DTE_ERR_HIP;
     if (n < 0 || n > capacity || (n > 0 && (!idx || !val))) return DTE_ERR_ARG;
-    const std::vector<Segment> sg = to_segments(segs, nseg);
     const std::string d(dir);
     if (!make_dir(d) || !make_dir(vdir(d, version))) return DTE_ERR_IO;
     std::vector<ChunkMeta> metas;
-    if (n == 0 || nseg == 0) {
-        if (n > 0) return DTE_ERR_ARG;   // entries but no segment to hold them
+    const int32_t npc = (int32_t)pcs.size();
+    if (n == 0 || npc == 0) {
+        if (n > 0) return DTE_ERR_ARG;   // entries but no piece to hold them
         fill_stats(stats, metas);
         return write_part_file(d, version, writer, sg, *opt, metas, 0);
     }
-    // segment bounds of the ordered delta, and local indices, on the device
-    std::vector<int64_t> hb((size_t)nseg), he((size_t)nseg);
-    for (int32_t i = 0; i < nseg; ++i) {
-        hb[i] = sg[i].begin;
-        he[i] = sg[i].begin + sg[i].numel;
+    // piece bounds of the ordered delta, and canonical local indices, on the device
+    std::vector<int64_t> hb((size_t)npc), he((size_t)npc);
+    for (int32_t i = 0; i < npc; ++i) {
+        hb[i] = pcs[i].begin;
+        he[i] = pcs[i].end;
     }
-    DevBuf dbeg, dend, dlo, dhi, dlocal, dbad;
-    const size_t sb = (size_t)nseg * sizeof(int64_t);
+    DevBuf dbeg, dend, dlo, dhi, dlocal, dbad, dpcs;
+    const size_t sb = (size_t)npc * sizeof(int64_t);
     if (!dbeg.alloc(sb) || !dend.alloc(sb) || !dlo.alloc(sb) || !dhi.alloc(sb) ||
-        !dlocal.alloc((size_t)n * sizeof(uint32_t)) || !dbad.alloc(sizeof(int32_t)))
+        !dlocal.alloc((size_t)n * sizeof(uint32_t)) || !dbad.alloc(sizeof(int32_t)) ||
+        !dpcs.alloc((size_t)npc * sizeof(Piece)))
         return DTE_ERR_HIP;
     int32_t* bad = static_cast<int32_t*>(dbad.p);
     const int32_t zero = 0;
-    if (hipMemcpyAsync(bad, &zero, sizeof zero, hipMemcpyHostToDevice, s) != hipSuccess)
-        return DTE_ERR_HIP;
     int64_t* b = static_cast<int64_t*>(dbeg.p);
     int64_t* en = static_cast<int64_t*>(dend.p);
     int64_t* lo_d = static_cast<int64_t*>(dlo.p);
     int64_t* hi_d = static_cast<int64_t*>(dhi.p);
     uint32_t* loc = static_cast<uint32_t*>(dlocal.p);
-    if (hipMemcpyAsync(b, hb.data(), sb, hipMemcpyHostToDevice, s) != hipSuccess ||
-        hipMemcpyAsync(en, he.data(), sb, hipMemcpyHostToDevice, s) != hipSuccess)
+    Piece* pd = static_cast<Piece*>(dpcs.p);
+    if (hipMemcpyAsync(bad, &zero, sizeof zero, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(b, hb.data(), sb, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(en, he.data(), sb, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(pd, pcs.data(), (size_t)npc * sizeof(Piece), hipMemcpyHostToDevice, s) !=
+            hipSuccess)
         return DTE_ERR_HIP;
-    hipLaunchKernelGGL(bounds_kernel, dim3((unsigned)((nseg + 255) / 256)), dim3(256), 0, s, idx, n,
-                       b, en, nseg, lo_d, hi_d);
+    hipLaunchKernelGGL(bounds_kernel, dim3((unsigned)((npc + 255) / 256)), dim3(256), 0, s, idx, n, b,
+                       en, npc, lo_d, hi_d);
     const int64_t want = (n + 255) / 256;
     const int64_t cap = (int64_t)device_cus() * 8;
     hipLaunchKernelGGL(narrow_kernel, dim3((unsigned)std::min(want, cap)), dim3(256), 0, s, idx, n, b,
-                       nseg, loc);
+                       pd, npc, loc);
     hipLaunchKernelGGL(ascending_kernel, dim3((unsigned)std::min(want, cap)), dim3(256), 0, s, idx, n,
                        bad);
-    std::vector<int64_t> lo((size_t)nseg), hi((size_t)nseg);
+    std::vector<int64_t> lo((size_t)npc), hi((size_t)npc);
     int32_t unordered = 0;
     if (hipGetLastError() != hipSuccess ||
         hipMemcpyAsync(lo.data(), lo_d, sb, hipMemcpyDeviceToHost, s) != hipSuccess ||
@@ -1016,11 +1094,14 @@ dte_status dte_store_write_part_device(const char* dir, int64_t version, int32_t
         return DTE_ERR_HIP;
     if (unordered) return DTE_ERR_ARG;     // not the output of an ordered extract
     int64_t inside = 0;
-    for (int32_t i = 0; i < nseg; ++i) inside += hi[i] - lo[i];
-    if (inside != n) return DTE_ERR_ARG;   // entries outside every segment (or not ascending)
-    const std::vector<ChunkJob> jobs = plan_chunks(lo, hi, opt->chunk_entries);
-    int64_t biggest = 1;
-    for (const ChunkJob& j : jobs) biggest = std::max(biggest, j.count);
+    for (int32_t i = 0; i < npc; ++i) inside += hi[i] - lo[i];
+    if (inside != n) return DTE_ERR_ARG;   // entries outside every piece
+    const std::vector<ChunkJob> jobs = plan_chunks(pcs, lo, hi, opt->chunk_entries);
+    int64_t biggest = 1, published = 0;
+    for (const ChunkJob& j : jobs) {
+        biggest = std::max(biggest, j.count);
+        published += j.count;
+    }
     Ring ring(opt->threads + 2, biggest);
     if (!ring.ok()) return DTE_ERR_HIP;
     std::mutex mm;
@@ -1048,7 +1129,62 @@ dte_status dte_store_write_part_device(const char* dir, int64_t version, int32_t
     }
     if (err.get() != DTE_OK) return err.get();
     fill_stats(stats, metas);
-    return write_part_file(d, version, writer, sg, *opt, metas, n);
+    return write_part_file(d, version, writer, sg, *opt, metas, published);
+}
+
+}  // namespace
+
+extern "C" {
+
+dte_status dte_store_write_part_host(const char* dir, int64_t version, int32_t writer,
+                                     const dte_store_segment* segs, int32_t nseg,
+                                     const int64_t* idx, const uint16_t* val, int64_t count,
+                                     const dte_store_options* opt, dte_store_stats* stats)
+{
+    if (!common_write_args(dir, version, writer, segs, nseg, opt)) return DTE_ERR_ARG;
+    const std::vector<Segment> sg = to_segments(segs, nseg);
+    return write_host_impl(dir, version, writer, sg, identity_pieces(sg), idx, val, count, opt, stats);
+}
+
+dte_status dte_store_write_part_host_mapped(const char* dir, int64_t version, int32_t writer,
+                                            const dte_store_segment* segs, int32_t nseg,
+                                            const dte_store_piece* pieces, int32_t npiece,
+                                            const int64_t* idx, const uint16_t* val, int64_t count,
+                                            const dte_store_options* opt, dte_store_stats* stats)
+{
+    if (!common_write_args(dir, version, writer, segs, nseg, opt) || npiece < 0 ||
+        (npiece > 0 && !pieces))
+        return DTE_ERR_ARG;
+    return write_host_impl(dir, version, writer, to_segments(segs, nseg), to_pieces(pieces, npiece),
+                           idx, val, count, opt, stats);
+}
+
+dte_status dte_store_write_part_device(const char* dir, int64_t version, int32_t writer,
+                                       const dte_store_segment* segs, int32_t nseg,
+                                       const int64_t* idx, const uint16_t* val,
+                                       const int64_t* count, int64_t capacity,
+                                       const dte_store_options* opt, dte_store_stats* stats,
+                                       void* stream)
+{
+    if (!common_write_args(dir, version, writer, segs, nseg, opt)) return DTE_ERR_ARG;
+    const std::vector<Segment> sg = to_segments(segs, nseg);
+    return write_device_impl(dir, version, writer, sg, identity_pieces(sg), idx, val, count, capacity,
+                             opt, stats, stream);
+}
+
+dte_status dte_store_write_part_device_mapped(const char* dir, int64_t version, int32_t writer,
+                                              const dte_store_segment* segs, int32_t nseg,
+                                              const dte_store_piece* pieces, int32_t npiece,
+                                              const int64_t* idx, const uint16_t* val,
+                                              const int64_t* count, int64_t capacity,
+                                              const dte_store_options* opt, dte_store_stats* stats,
+                                              void* stream)
+{
+    if (!common_write_args(dir, version, writer, segs, nseg, opt) || npiece < 0 ||
+        (npiece > 0 && !pieces))
+        return DTE_ERR_ARG;
+    return write_device_impl(dir, version, writer, to_segments(segs, nseg), to_pieces(pieces, npiece),
+                             idx, val, count, capacity, opt, stats, stream);
 }
 
 dte_status dte_store_commit(const char* dir, int64_t version, int64_t parent, int32_t nwriters,
@@ -1092,13 +1228,6 @@ dte_status dte_store_commit(const char* dir, int64_t version, int64_t parent, in
         entries += e;
         chunks.insert(chunks.end(), pc.begin(), pc.end());
     }
-    // partitions are disjoint: one writer per segment
-    std::map<int32_t, int32_t> owner;
-    for (const ChunkMeta& c : chunks) {
-        auto it = owner.find(c.segment);
-        if (it != owner.end() && it->second != c.writer) return DTE_ERR_ARG;
-        owner[c.segment] = c.writer;
-    }
     if (entries == 0) {   // no changed payload anywhere: no new version
         if (DIR* dd = opendir(vd.c_str())) {
             while (dirent* de = readdir(dd)) {
@@ -1111,7 +1240,8 @@ dte_status dte_store_commit(const char* dir, int64_t version, int64_t parent, in
         return DTE_OK;
     }
     std::sort(chunks.begin(), chunks.end(), [](const ChunkMeta& a, const ChunkMeta& b) {
-        return a.segment != b.segment ? a.segment < b.segment : a.first < b.first;
+        if (a.segment != b.segment) return a.segment < b.segment;
+        return a.writer != b.writer ? a.writer < b.writer : a.first < b.first;
     });
     std::string s = "{\"format\": \"dte-delta-1\", \"version\": " + std::to_string(version) +
                     ", \"parent\": " + std::to_string(parent) + ", \"codec\": \"" + codec +

@@ -346,3 +346,32 @@ def build_spec(wl) -> PlanSpec:
         placed.append(lst)
         numel.append(base)
     return PlanSpec(segments, placed, numel, senders)
+
+
+def store_pieces(wl):
+    """The trainer shard as pieces of canonical tensors for the storage
+    path (dte_store_piece rows: sender_begin, sender_end, segment,
+    local_cols, canon_cols, canon_row0, canon_col0).  Every sender piece
+    covers whole rows of its segment.  Tensors that every tensor-parallel
+    rank holds whole (the norms) are published by rank 0 only."""
+    rows, pos = [], 0
+    replicated = wl.sender.kind == "mcore" and wl.sender.tp > 1
+    for sg in sender_segments(wl):
+        numel = 1
+        for x in sg.shape:
+            numel *= x
+        cols = sg.shape[-1] if len(sg.shape) == 2 else numel
+        for sp in sorted(sg.pieces, key=lambda x: x.local_lo):
+            t = wl.tensors[sp.tensor]
+            if len(sg.shape) == 2:
+                if sp.extent[1] != cols or sp.local_lo[1] != 0:
+                    raise ValueError("store pieces must cover whole rows of %s" % sg.name)
+                b = pos + sp.local_lo[0] * cols
+                e = b + sp.extent[0] * cols
+                owner = sp.tensor
+                rows.append((b, e, owner, cols, t.shape[1], sp.canon_lo[0], sp.canon_lo[1]))
+            else:
+                owner = sp.tensor if not (replicated and wl.sender.rank != 0) else -1
+                rows.append((pos, pos + numel, owner, numel, numel, 0, 0))
+        pos += numel
+    return rows

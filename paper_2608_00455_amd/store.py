@@ -29,12 +29,21 @@ class dte_store_options(ctypes.Structure):
                 ("chunk_entries", ctypes.c_int64)]
 
 
+class dte_store_piece(ctypes.Structure):
+    _fields_ = [("sender_begin", ctypes.c_int64), ("sender_end", ctypes.c_int64),
+                ("segment", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("local_cols", ctypes.c_int64), ("canon_cols", ctypes.c_int64),
+                ("canon_row0", ctypes.c_int64), ("canon_col0", ctypes.c_int64)]
+
+
 class dte_store_stats(ctypes.Structure):
     _fields_ = [("entries", ctypes.c_int64), ("chunks", ctypes.c_int64),
                 ("raw_bytes", ctypes.c_int64), ("stored_bytes", ctypes.c_int64)]
 
 
-EXPORTED = ("dte_store_write_part_host", "dte_store_write_part_device", "dte_store_commit",
+EXPORTED = ("dte_store_write_part_host", "dte_store_write_part_device",
+            "dte_store_write_part_host_mapped", "dte_store_write_part_device_mapped",
+            "dte_store_commit",
             "dte_store_latest", "dte_store_chain", "dte_store_read_host",
             "dte_store_read_device", "dte_store_xxh64")
 
@@ -55,6 +64,13 @@ def _lib():
         L.dte_store_write_part_device.restype = S
         L.dte_store_write_part_device.argtypes = [ctypes.c_char_p, I64, I32, seg_p, I32, P, P, P,
                                                   I64, opt_p, st_p, P]
+        pc_p = ctypes.POINTER(dte_store_piece)
+        L.dte_store_write_part_host_mapped.restype = S
+        L.dte_store_write_part_host_mapped.argtypes = [ctypes.c_char_p, I64, I32, seg_p, I32, pc_p,
+                                                       I32, P, P, I64, opt_p, st_p]
+        L.dte_store_write_part_device_mapped.restype = S
+        L.dte_store_write_part_device_mapped.argtypes = [ctypes.c_char_p, I64, I32, seg_p, I32,
+                                                         pc_p, I32, P, P, P, I64, opt_p, st_p, P]
         L.dte_store_commit.restype = S
         L.dte_store_commit.argtypes = [ctypes.c_char_p, I64, I64, I32, ctypes.POINTER(I32)]
         L.dte_store_latest.restype = S
@@ -114,29 +130,53 @@ def _dir(d) -> bytes:
     return str(d).encode()
 
 
+def pieces_of(rows):
+    """Host array of dte_store_piece from tuples (sender_begin, sender_end,
+    segment, local_cols, canon_cols, canon_row0, canon_col0)."""
+    arr = (dte_store_piece * max(1, len(rows)))()
+    for i, (b, e, sg, lc, cc, r0, c0) in enumerate(rows):
+        arr[i] = dte_store_piece(b, e, sg, 0, lc, cc, r0, c0)
+    return arr, len(rows)
+
+
 def write_part_host(d, version, writer, segs, idx: np.ndarray, val: np.ndarray,
-                    opt: Options = Options()) -> Stats:
+                    opt: Options = Options(), pieces=None) -> Stats:
     arr, nseg, _keep = segs
     idx = np.ascontiguousarray(idx, dtype=np.int64)
     val = np.ascontiguousarray(val, dtype=np.uint16)
     st = dte_store_stats()
-    B._check("dte_store_write_part_host",
-             _lib().dte_store_write_part_host(_dir(d), version, writer, arr, nseg,
-                                              idx.ctypes.data if idx.size else None,
-                                              val.ctypes.data if val.size else None, idx.size,
-                                              ctypes.byref(opt.c()), ctypes.byref(st)))
+    ip = idx.ctypes.data if idx.size else None
+    vp = val.ctypes.data if val.size else None
+    if pieces is None:
+        rc = _lib().dte_store_write_part_host(_dir(d), version, writer, arr, nseg, ip, vp,
+                                              idx.size, ctypes.byref(opt.c()), ctypes.byref(st))
+    else:
+        parr, npc = pieces
+        rc = _lib().dte_store_write_part_host_mapped(_dir(d), version, writer, arr, nseg, parr,
+                                                     npc, ip, vp, idx.size,
+                                                     ctypes.byref(opt.c()), ctypes.byref(st))
+    B._check("dte_store_write_part_host", rc)
     return _stats(st)
 
 
 def write_part_device(d, version, writer, segs, idx_ptr: int, val_ptr: int, count_ptr: int,
-                      capacity: int, opt: Options = Options(), stream: int = 0) -> Stats:
+                      capacity: int, opt: Options = Options(), stream: int = 0,
+                      pieces=None) -> Stats:
     arr, nseg, _keep = segs
     st = dte_store_stats()
-    B._check("dte_store_write_part_device",
-             _lib().dte_store_write_part_device(_dir(d), version, writer, arr, nseg,
+    if pieces is None:
+        rc = _lib().dte_store_write_part_device(_dir(d), version, writer, arr, nseg,
                                                 idx_ptr or None, val_ptr or None, count_ptr,
                                                 capacity, ctypes.byref(opt.c()),
-                                                ctypes.byref(st), stream or None))
+                                                ctypes.byref(st), stream or None)
+    else:
+        parr, npc = pieces
+        rc = _lib().dte_store_write_part_device_mapped(_dir(d), version, writer, arr, nseg, parr,
+                                                       npc, idx_ptr or None, val_ptr or None,
+                                                       count_ptr, capacity,
+                                                       ctypes.byref(opt.c()), ctypes.byref(st),
+                                                       stream or None)
+    B._check("dte_store_write_part_device", rc)
     return _stats(st)
 
 

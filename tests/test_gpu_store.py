@@ -15,7 +15,7 @@ from oracle import run as orun
 from paper_2608_00455_amd import binding as B
 from paper_2608_00455_amd import layouts
 from paper_2608_00455_amd import store as S
-from paper_2608_00455_amd.pipeline import DeltaPipeline
+from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state
 from synth import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -95,3 +95,48 @@ def test_unordered_device_delta_is_refused(tmp_path):
                             pipe.val.data_ptr(), pipe.cursor.data_ptr(), pipe.capacity)
     assert e.value.status == B.DTE_ERR_ARG
     pipe.close()
+
+
+def test_megatron_core_ranks_publish_from_device(tmp_path):
+    """Two tensor-parallel Megatron-Core trainer ranks each extract their
+    own shard (ordered) and publish it mapped to canonical tensors; the
+    destination reads the version into device memory, remaps and applies
+    it with the canonical model's receiver plan: the shards then hold the
+    new BF16 weights everywhere."""
+    wl0 = W.scaled_mcore(layers=2, trainer_tp=2, trainer_rank=0, receiver_tp=4, vocab=64,
+                         lr=1e-5)
+    twin = W.canonical_twin(wl0)
+    say("case: store from mcore ranks", wl0.name)
+    res = orun.extract(twin, keep=("ph", "p"))
+    d = tmp_path / "store"
+    segs = segs_of(twin)
+    for r in range(2):
+        wl = W.with_sender_rank(wl0, r)
+        p, m, v = generate_state(wl)
+        spec = layouts.build_spec(wl)
+        pipe = DeltaPipeline(spec, capacity=p.numel(), ordered=True)
+        pipe.reset()
+        pipe.extract(p, m, v, wl.hp)
+        S.write_part_device(d, 1, r, segs, pipe.idx.data_ptr(), pipe.val.data_ptr(),
+                            pipe.cursor.data_ptr(), pipe.capacity, S.Options(chunk_entries=2000),
+                            torch.cuda.current_stream().cuda_stream,
+                            pieces=S.pieces_of(layouts.store_pieces(wl)))
+        pipe.close()
+    assert S.commit(d, 1, 0, 2)
+    pl = oplan.build_plan(twin)
+    old = oremap.layout(pl, ocore.bf16(orun.flat(res.parts, "ph")))
+    new = oremap.layout(pl, ocore.bf16(orun.flat(res.parts, "p")))
+    dst = DeltaPipeline(layouts.build_spec(twin), capacity=res.idx.size,
+                        shards=[dev(x.view(np.int16)) for x in old])
+    n, _ = S.read_device(d, 1, 0, dst.idx.data_ptr(), dst.val.data_ptr(), dst.capacity,
+                         stream=torch.cuda.current_stream().cuda_stream)
+    assert n == res.idx.size
+    dst.cursor.fill_(n)
+    idx, val, _ = dst.delta()
+    assert np.array_equal(idx, res.idx) and np.array_equal(val, res.val)
+    dst.remap()
+    dst.apply()
+    torch.cuda.synchronize()
+    for r in range(pl.nranks):
+        assert np.array_equal(dst.shards[r].cpu().numpy().view(np.uint16), new[r]), r
+    dst.close()

@@ -6,8 +6,9 @@ ctypes), independent of the library's own reader; the payload is the
 oracle's delta, and the destination's result (oracle remap and apply of
 what was read) is the receiver layout of the new BF16 weights.  Commit
 rules: no version without a changed entry, a missing writer part publishes
-nothing, partitions are disjoint, the version chain is followed from
-parents, and corrupted or truncated chunks are rejected.
+nothing, several writers may hold entries of one tensor (tensor-parallel
+Megatron-Core ranks publish their pieces of it), the version chain is
+followed from parents, and corrupted or truncated chunks are rejected.
 """
 import ctypes
 import json
@@ -146,13 +147,17 @@ def test_two_writers_disjoint_partitions(tmp_path, delta):
     assert S.commit(d, 1, 0, 2)
     idx, val, _ = S.read_host(d, 1, 0)
     assert np.array_equal(idx, res.idx) and np.array_equal(val, res.val)
-    # a segment written by two writers is rejected
-    S.write_part_host(d, 2, 0, segs_of(wl), res.idx, res.val)
-    S.write_part_host(d, 2, 1, segs_of(wl), res.idx[~lo], res.val[~lo])
-    with pytest.raises(B.DteError) as e:
-        S.commit(d, 2, 1, 2)
-    assert e.value.status == B.DTE_ERR_ARG
-    assert S.latest(d) == 1
+    # both writers with entries of every segment (even / odd entries): the
+    # version holds the union, grouped by segment then writer
+    even = np.arange(res.idx.size) % 2 == 0
+    S.write_part_host(d, 2, 0, segs_of(wl), res.idx[even], res.val[even])
+    S.write_part_host(d, 2, 1, segs_of(wl), res.idx[~even], res.val[~even])
+    assert S.commit(d, 2, 1, 2)
+    idx, val, _ = S.read_host(d, 2, 1)
+    srt = np.argsort(idx, kind="stable")
+    assert np.array_equal(idx[srt], res.idx) and np.array_equal(val[srt], res.val)
+    seg = np.searchsorted(np.array(begins), idx, side="right") - 1
+    assert np.all(np.diff(seg) >= 0)
 
 
 def test_version_chain(tmp_path, delta):
@@ -208,3 +213,54 @@ def test_writer_rejects_bad_input(tmp_path, delta):
         S.write_part_host(d, 1, 0, segs, res.idx, res.val, S.Options(threads=0))
     with pytest.raises(B.DteError):               # version 0
         S.write_part_host(d, 0, 0, segs, res.idx, res.val)
+
+
+def _mcore_delta_in_sender_offsets(wl):
+    """The oracle's delta of the rank's elements (sec. 3.2.1, in canonical
+    offsets) expressed as offsets of the rank's own shard, ascending."""
+    from oracle import mcore
+    ci = mcore.canonical_index(wl)
+    res = mcore.extract(wl)
+    order = np.argsort(ci, kind="stable")
+    sender = order[np.searchsorted(ci[order], res.idx)]
+    srt = np.argsort(sender, kind="stable")
+    return sender[srt], res.val[srt]
+
+
+def test_megatron_core_writers_publish_the_canonical_delta(tmp_path):
+    """Two tensor-parallel trainer ranks of a Megatron-Core shard publish
+    their changes mapped to canonical tensors (norms by rank 0 only); the
+    committed version holds exactly the canonical model's delta."""
+    from paper_2608_00455_amd import layouts
+    wl0 = W.scaled_mcore(trainer_tp=2, trainer_rank=0, vocab=64, lr=1e-5)
+    twin = W.canonical_twin(wl0)
+    segs = segs_of(twin)
+    d = tmp_path / "store"
+    for r in range(2):
+        wl = W.with_sender_rank(wl0, r)
+        idx, val = _mcore_delta_in_sender_offsets(wl)
+        pieces = S.pieces_of(layouts.store_pieces(wl))
+        S.write_part_host(d, 1, r, segs, idx, val, S.Options(chunk_entries=300), pieces=pieces)
+    assert S.commit(d, 1, 0, 2)
+    idx, val, _ = S.read_host(d, 1, 0)
+    want = orun.extract(twin, threads=2)
+    srt = np.argsort(idx, kind="stable")
+    assert np.array_equal(idx[srt], want.idx) and np.array_equal(val[srt], want.val)
+    man, idx2, val2 = independent_read(str(d), 1)
+    assert sorted({c["writer"] for c in man["chunks"]}) == [0, 1]
+    srt2 = np.argsort(idx2, kind="stable")
+    assert np.array_equal(idx2[srt2], want.idx)
+
+
+def test_mapped_writer_rejects_overlapping_or_unmapped_entries(tmp_path, delta):
+    wl, res = delta
+    segs = segs_of(wl)
+    n0 = wl.tensors[0].numel
+    # two pieces claiming the same sender range
+    bad = S.pieces_of([(0, n0, 0, n0, n0, 0, 0), (0, n0, 0, n0, n0, 0, 0)])
+    with pytest.raises(B.DteError):
+        S.write_part_host(tmp_path / "a", 1, 0, segs, res.idx[:1], res.val[:1], pieces=bad)
+    # entries outside every piece
+    only_first = S.pieces_of([(0, n0, 0, n0, n0, 0, 0)])
+    with pytest.raises(B.DteError):
+        S.write_part_host(tmp_path / "b", 1, 0, segs, res.idx, res.val, pieces=only_first)

@@ -185,6 +185,9 @@ def main():
     ap.add_argument("--lr", type=float, default=None)
     ap.add_argument("--literal", action="store_true",
                     help="literal operation order of the AdamW inverse (four divisions)")
+    ap.add_argument("--fused", action="store_true",
+                    help="dte_extract_remap (detection routed straight into the buckets) "
+                         "instead of dte_extract_delta + dte_remap")
     ap.add_argument("--ordered", action="store_true",
                     help="dte_extract_delta_ordered (ascending, deterministic delta)")
     ap.add_argument("--norm-group", action="store_true",
@@ -253,18 +256,32 @@ def main():
             if ev:
                 ev[1].record(stream)
             return
-        pipe.reset()
-        if ev:
-            ev[0].record(stream)
-        if len(runs) == 1:
-            pipe.extract(p, m, v, hp)
+        if args.fused:
+            pipe.cursor.zero_()
+            pipe.rank_count.zero_()
+            if ev:
+                ev[0].record(stream)
+            for b, e, h in runs:
+                if len(runs) == 1:
+                    pipe.extract_remap(p, m, v, h)
+                else:
+                    pipe.extract_remap(p[b:e], m[b:e], v[b:e], h, n=e - b, index_base=b)
+            if ev:
+                ev[1].record(stream)
+                ev[2].record(stream)
         else:
-            pipe.extract_runs(p, m, v, runs)
-        if ev:
-            ev[1].record(stream)
-        pipe.remap()
-        if ev:
-            ev[2].record(stream)
+            pipe.reset()
+            if ev:
+                ev[0].record(stream)
+            if len(runs) == 1:
+                pipe.extract(p, m, v, hp)
+            else:
+                pipe.extract_runs(p, m, v, runs)
+            if ev:
+                ev[1].record(stream)
+            pipe.remap()
+            if ev:
+                ev[2].record(stream)
         pipe.apply()
         if ev:
             ev[3].record(stream)
@@ -305,12 +322,19 @@ def main():
         rem_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
         app_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
         k_ms = ext_ms
-        k_bytes = 12 * n + 10 * changed       # read theta, m, v; write (idx, val)
+        if args.fused:                        # read theta, m, v; write (offset, value) per route
+            k_bytes = 12 * n + 10 * routed
+        else:                                 # read theta, m, v; write (idx, val)
+            k_bytes = 12 * n + 10 * changed
         value = n / (ms_step / 1e3)
         metric_unit = "elements/s"
-        kernel = "extract"
-    step_bytes = (k_bytes if apply_only else
-                  12 * n + 10 * changed + 10 * changed + 10 * routed + 12 * routed)
+        kernel = "extract_remap" if args.fused else "extract"
+    if apply_only:
+        step_bytes = k_bytes
+    elif args.fused:
+        step_bytes = 12 * n + 10 * routed + 12 * routed
+    else:
+        step_bytes = 12 * n + 10 * changed + 10 * changed + 10 * routed + 12 * routed
     achieved = k_bytes / (k_ms / 1e3) / 1e9
     out = {
         "metric": "delta-extract+remap+apply: elements/s and HBM GB/s (% of peak), "
@@ -327,7 +351,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
         "config": {"workload": wl.name, "elements": n, "changed": changed, "extract_calls": len(runs), "settle_s": args.settle,
-                   "ordered": bool(args.ordered), "order": "literal" if args.literal else "folded",
+                   "ordered": bool(args.ordered), "fused": bool(args.fused), "order": "literal" if args.literal else "folded",
                    "change_fraction": c, "receiver_ranks": len(counts),
                    "routed_entries": routed, "lr": hp.lr,
                    "step_algorithmic_bytes": step_bytes,

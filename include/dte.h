@@ -251,6 +251,22 @@ dte_status dte_remap(const dte_plan* plan, const int64_t* idx, const uint16_t* v
                      uint16_t* const* out_val, const int64_t* rank_capacity,
                      int64_t* rank_count, void* stream);
 
+/* dte_extract_delta and dte_remap in one pass (paper sec. 3.2.1: changed
+ * indices are remapped as soon as they are detected): the changed entries
+ * of [index_base, index_base + n) are routed through `plan` straight into
+ * the receiver buckets, without the (I, V) arrays.  Arguments as in those
+ * two calls; the plan has at most 16 ranks.  Unlike dte_remap, rank_count
+ * is not cleared: each call adds its routed entries to it (and to *count,
+ * device int64, the number of changed entries), so one step over several
+ * parameter-group ranges clears both once, before its first call.  Entries
+ * beyond rank_capacity[r] are dropped and counted; bucket order is
+ * unspecified.  No theta_hat output.  Errors: DTE_ERR_ARG, DTE_ERR_HIP. */
+dte_status dte_extract_remap(const float* p, const float* m, const float* v, int64_t n,
+                             int64_t index_base, const dte_adamw_step* hp, const dte_plan* plan,
+                             int64_t* const* out_off, uint16_t* const* out_val,
+                             const int64_t* rank_capacity, int64_t* rank_count, int64_t* count,
+                             void* stream);
+
 /* Direct sparse apply (paper sec. 3.3, eq. direct_sparse_apply):
  * shards[r][off[r][k]] = val[r][k] for k < min(rank_count[r],
  * rank_capacity[r]), every rank r.  Because values are targets, applying a

@@ -18,7 +18,8 @@ DTE_MAX_RANKS = 64
 
 EXPORTED = ("dte_derive_scalars", "dte_extract_delta", "dte_ordered_workspace_bytes",
             "dte_extract_delta_ordered", "dte_plan_create", "dte_plan_destroy",
-            "dte_plan_info", "dte_remap", "dte_apply", "dte_adamw_forward", "dte_status_string")
+            "dte_plan_info", "dte_remap", "dte_extract_remap", "dte_apply", "dte_adamw_forward",
+            "dte_status_string")
 
 
 class DteError(RuntimeError):
@@ -93,6 +94,10 @@ def _lib():
         L.dte_remap.restype = S
         L.dte_remap.argtypes = [P, P, P, P, I64, ctypes.POINTER(P), ctypes.POINTER(P),
                                 ctypes.POINTER(I64), P, P]
+        L.dte_extract_remap.restype = S
+        L.dte_extract_remap.argtypes = [P, P, P, I64, I64, ctypes.POINTER(dte_adamw_step), P,
+                                        ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(I64),
+                                        P, P, P]
         L.dte_apply.restype = S
         L.dte_apply.argtypes = [P, ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(P), P,
                                 ctypes.POINTER(I64), P]
@@ -151,6 +156,14 @@ def dte_extract_delta_ordered(p, m, v, n, index_base, hp, out_idx, out_val, capa
                                             out_idx, out_val, capacity, cursor,
                                             workspace or None, workspace_bytes,
                                             out_prev or None, stream or None))
+
+
+def dte_extract_remap(p, m, v, n, index_base, hp, plan, out_off, out_val, rank_capacity,
+                      rank_count, count, stream=0):
+    _check("dte_extract_remap",
+           _lib().dte_extract_remap(p, m, v, n, index_base, ctypes.byref(_hp(hp)), plan,
+                                    _ptrs(out_off), _ptrs(out_val), _i64s(rank_capacity),
+                                    rank_count, count, stream or None))
 
 
 def dte_adamw_forward(p, m, v, g, n, hp, stream=0):

@@ -340,6 +340,7 @@ dte::ExtractParams extract_params(const float* p, const float* m, const float* v
     a.cursor = cursor;
     a.out_prev = out_prev;
     a.runs = nullptr;
+    a.route = 0;
     return a;
 }
 
@@ -627,6 +628,40 @@ dte_status dte_remap(const dte_plan* plan, const int64_t* idx, const uint16_t* v
             return DTE_ERR_HIP;
     }
     return DTE_OK;
+}
+
+dte_status dte_extract_remap(const float* p, const float* m, const float* v, int64_t n,
+                             int64_t index_base, const dte_adamw_step* hp, const dte_plan* plan,
+                             int64_t* const* out_off, uint16_t* const* out_val,
+                             const int64_t* rank_capacity, int64_t* rank_count, int64_t* count,
+                             void* stream)
+{
+    if (!plan || !out_off || !out_val || !rank_capacity || !rank_count ||
+        plan->nranks > dte::kRanksPerLaunch)
+        return DTE_ERR_ARG;
+    if (!extract_args_ok(p, m, v, n, index_base, hp, nullptr, nullptr, 0, count))
+        return DTE_ERR_ARG;
+    for (int32_t r = 0; r < plan->nranks; ++r) {
+        if (rank_capacity[r] < 0) return DTE_ERR_ARG;
+        if (rank_capacity[r] > 0 && (!out_off[r] || !out_val[r])) return DTE_ERR_ARG;
+    }
+    if (n == 0) return DTE_OK;
+    dte::ExtractParams a = extract_params(p, m, v, n, index_base, hp, nullptr, nullptr, 0, count,
+                                          nullptr);
+    a.route = 1;
+    a.plan = plan->view;
+    std::memset(&a.out, 0, sizeof a.out);
+    a.out.first = 0;
+    a.out.count = plan->nranks;
+    for (int32_t r = 0; r < plan->nranks; ++r) {
+        a.out.off[r] = out_off[r];
+        a.out.val[r] = out_val[r];
+        a.out.cap[r] = rank_capacity[r];
+    }
+    a.rank_count = rank_count;
+    return dte::launch_extract(a, cu_count(plan->device), (hipStream_t)stream) == hipSuccess
+               ? DTE_OK
+               : DTE_ERR_HIP;
 }
 
 dte_status dte_apply(const dte_plan* plan, uint16_t* const* shards, const int64_t* const* off,

@@ -9,6 +9,41 @@
 
 namespace dte {
 
+// ---- transfer plan on the device ----------------------------------------
+
+constexpr int kRanksPerLaunch = 16;   // per-rank pointers travel as kernel arguments
+
+struct DevOp {
+    int64_t dst_base;
+    int32_t rank;
+    int32_t ndim;
+    uint32_t src_origin[DTE_MAX_DIMS];
+    uint32_t extent[DTE_MAX_DIMS];
+    uint32_t dst_origin[DTE_MAX_DIMS];
+    uint32_t dst_shape[DTE_MAX_DIMS];
+};
+
+struct PlanView {
+    const int64_t* seg_begin;   // nseg + 1 (last = total)
+    const uint32_t* seg_shape;  // nseg * DTE_MAX_DIMS
+    const int32_t* seg_ndim;    // nseg
+    const int32_t* seg_ops;     // nseg + 1, CSR into ops (by segment)
+    const DevOp* ops;           // nop
+    const int32_t* lookup;      // nbuckets: segment holding element (b << shift)
+    int64_t total;
+    int64_t nbuckets;
+    int32_t nseg;
+    int32_t shift;
+};
+
+struct RankSlice {                 // ranks [first, first + count) of one launch
+    int32_t first;
+    int32_t count;
+    int64_t* off[kRanksPerLaunch];
+    uint16_t* val[kRanksPerLaunch];
+    int64_t cap[kRanksPerLaunch];
+};
+
 // ---- extract (fused AdamW inverse + BF16 detection + compaction) --------
 
 // One flush of one wave in ordered mode: `count` entries written at
@@ -46,6 +81,13 @@ struct ExtractParams {
     int64_t* run_cursor;
     int64_t* wave_count;
     int32_t wave0;        // global number of this launch's first wave
+    // routing mode (route != 0): each flush sends its entries through the
+    // plan into the receiver buckets (out, counts added to rank_count)
+    // instead of writing (out_idx, out_val); the cursor still counts them
+    int32_t route;
+    PlanView plan;
+    RankSlice out;
+    int64_t* rank_count;
 };
 
 // Largest number of waves one extract call launches in ordered mode.
@@ -91,41 +133,6 @@ struct ForwardParams {
 };
 
 hipError_t launch_adamw_forward(const ForwardParams& a, int cus, hipStream_t stream);
-
-// ---- transfer plan on the device ----------------------------------------
-
-constexpr int kRanksPerLaunch = 16;   // per-rank pointers travel as kernel arguments
-
-struct DevOp {
-    int64_t dst_base;
-    int32_t rank;
-    int32_t ndim;
-    uint32_t src_origin[DTE_MAX_DIMS];
-    uint32_t extent[DTE_MAX_DIMS];
-    uint32_t dst_origin[DTE_MAX_DIMS];
-    uint32_t dst_shape[DTE_MAX_DIMS];
-};
-
-struct PlanView {
-    const int64_t* seg_begin;   // nseg + 1 (last = total)
-    const uint32_t* seg_shape;  // nseg * DTE_MAX_DIMS
-    const int32_t* seg_ndim;    // nseg
-    const int32_t* seg_ops;     // nseg + 1, CSR into ops (by segment)
-    const DevOp* ops;           // nop
-    const int32_t* lookup;      // nbuckets: segment holding element (b << shift)
-    int64_t total;
-    int64_t nbuckets;
-    int32_t nseg;
-    int32_t shift;
-};
-
-struct RankSlice {                 // ranks [first, first + count) of one launch
-    int32_t first;
-    int32_t count;
-    int64_t* off[kRanksPerLaunch];
-    uint16_t* val[kRanksPerLaunch];
-    int64_t cap[kRanksPerLaunch];
-};
 
 hipError_t launch_zero_i64(int64_t* p, int64_t n, hipStream_t stream);
 

@@ -41,6 +41,7 @@
 #include <hip/hip_runtime.h>
 
 #include "dte_internal.h"
+#include "route.h"
 
 #pragma clang fp contract(off)
 
@@ -194,11 +195,51 @@ __device__ __forceinline__ void wave_sync()
 }
 
 // Copy a wave's staged LDS entries to the reserved global range (and, in
-// ordered mode, record the run).
+// ordered mode, record the run).  Routing mode: route them through the plan
+// into the receiver buckets instead (count, one reservation per rank, write).
+template <bool kRoute>
 __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging& so, int lane)
 {
     const int staged = so.staged;
     wave_sync();   // every lane's LDS stores visible to the other lanes
+    if (kRoute) {
+        if (lane == 0)
+            atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor), (unsigned long long)staged);
+        rt::SegInfo cache{0, 0, 0, 0, 0};
+        int runv = 0;                            // lane r: entries for rank out.first + r
+#pragma unroll 1
+        for (int pass = 0; pass < 2; ++pass) {
+            int64_t basev = 0;
+            if (pass == 1) {
+                if (lane < a.out.count && runv > 0)
+                    basev = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(
+                                                   &a.rank_count[a.out.first + lane]),
+                                               (unsigned long long)runv);
+                runv = 0;
+            }
+#pragma unroll 1
+            for (int g = 0; g < staged; g += 64) {
+                const int i = g + lane;
+                int64_t x = -1;
+                uint16_t y = 0;
+                if (i < staged) {
+                    const uint32_t key = st.key[i];
+                    const int64_t t = st.t_first + (int64_t)(key >> kTileBits);
+                    x = a.index_base + t * kWaveTile + (key & (kWaveTile - 1));
+                    y = st.val[i];
+                    if (x >= a.plan.total) x = -1;
+                }
+                if (pass == 0)
+                    rt::route_slot<false>(a.plan, a.out, lane, x, y, runv, 0, cache);
+                else
+                    rt::route_slot<true>(a.plan, a.out, lane, x, y, runv, basev, cache);
+            }
+        }
+        so.flushed += staged;
+        so.staged = 0;
+        wave_sync();
+        return;
+    }
     unsigned long long base = 0;
     if (lane == 0) {
         base = atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor),
@@ -263,6 +304,7 @@ __device__ __forceinline__ int lanes_before(const Slot4& r)
 
 // Stage one ballot of changed entries (at most 64), flushing first when the
 // staging area would overflow.  Wave-uniform control flow.
+template <bool kRoute>
 __device__ __forceinline__ void stage_changed(const ExtractParams& a, const WaveStage& st,
                                               Staging& so, int lane, bool changed,
                                               uint32_t key, uint16_t val)
@@ -270,7 +312,7 @@ __device__ __forceinline__ void stage_changed(const ExtractParams& a, const Wave
     const uint64_t k = __ballot(changed);
     if (k == 0) return;
     const int cnt = __popcll(k);
-    if (so.staged + cnt > kWaveStage) flush_wave(a, st, so, lane);
+    if (so.staged + cnt > kWaveStage) flush_wave<kRoute>(a, st, so, lane);
     if (changed) {
         const int pos = so.staged + lane_prefix(k);
         st.key[pos] = key;
@@ -281,7 +323,7 @@ __device__ __forceinline__ void stage_changed(const ExtractParams& a, const Wave
 
 // Exact inverse of every queued candidate, 64 per pass; changed ones are
 // staged.  Empties the queue.
-template <bool kDecayOne, bool kLit>
+template <bool kDecayOne, bool kLit, bool kRoute>
 __device__ void drain_queue(const ExtractParams& a, const WaveStage& st, int& queued, Staging& so,
                             int lane)
 {
@@ -298,7 +340,7 @@ __device__ void drain_queue(const ExtractParams& a, const WaveStage& st, int& qu
             changed = bf16_bits(ph) != bn;
             key = st.qkey[i];
         }
-        stage_changed(a, st, so, lane, changed, key, bn);
+        stage_changed<kRoute>(a, st, so, lane, changed, key, bn);
     }
     queued = 0;
     wave_sync();
@@ -329,7 +371,7 @@ __device__ __forceinline__ void load_tile(const ExtractParams& a, int64_t t0, in
     }
 }
 
-template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev, bool kLit>
+template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev, bool kLit, bool kRoute>
 __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0, int lane,
                                              Staging& so, int& queued, const WaveStage& st,
                                              uint32_t iter, const f32x4* P, const f32x4* M,
@@ -355,7 +397,7 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
             }
             const Slot4 r = select4(sel);
             if (r.count != 0) {
-                if (so.staged + r.count > kWaveStage) flush_wave(a, st, so, lane);
+                if (so.staged + r.count > kWaveStage) flush_wave<kRoute>(a, st, so, lane);
                 const int base = so.staged + lanes_before(r);
                 int k = 0;
 #pragma unroll
@@ -385,7 +427,7 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
             const Slot4 r = select4(sel);
             if (r.count != 0) {
                 if (queued + r.count > kQueue)
-                    drain_queue<kDecayOne, kLit>(a, st, queued, so, lane);
+                    drain_queue<kDecayOne, kLit, kRoute>(a, st, queued, so, lane);
                 const int base = queued + lanes_before(r);
                 int k = 0;
 #pragma unroll
@@ -405,7 +447,7 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
 }
 
 // Wave tiles [first, last) of the range; kFull: each lies inside [0, n).
-template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev, bool kLit>
+template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev, bool kLit, bool kRoute>
 __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_t first,
                                                          int64_t last)
 {
@@ -432,11 +474,11 @@ __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_
     for (int64_t t = w_first; t < w_last; ++t) {
         f32x4 P[kVec], M[kVec], V[kVec];
         load_tile<kFull, kVecLoads>(a, t * kWaveTile, lane, P, M, V);
-        process_tile<kFull, kVecLoads, kDecayOne, kWritePrev, kLit>(a, t * kWaveTile, lane, so,
+        process_tile<kFull, kVecLoads, kDecayOne, kWritePrev, kLit, kRoute>(a, t * kWaveTile, lane, so,
                                                              queued, st, iter++, P, M, V);
     }
-    if (queued > 0) drain_queue<kDecayOne, kLit>(a, st, queued, so, lane);
-    if (so.staged > 0) flush_wave(a, st, so, lane);
+    if (queued > 0) drain_queue<kDecayOne, kLit, kRoute>(a, st, queued, so, lane);
+    if (so.staged > 0) flush_wave<kRoute>(a, st, so, lane);
     if (a.runs && lane == 0) a.wave_count[st.wave] = so.flushed;
 }
 
@@ -486,7 +528,7 @@ __global__ __launch_bounds__(256) void adamw_forward_kernel(ForwardParams a)
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Launch over wave tiles [first, last); returns the number of waves.
-template <bool F, bool V, bool D, bool L>
+template <bool F, bool V, bool D, bool L, bool R>
 int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_grid,
                      int32_t wave0, hipStream_t s)
 {
@@ -494,25 +536,28 @@ int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_g
     const int64_t blocks = (last - first + kWaves - 1) / kWaves;
     const dim3 grid((unsigned)(blocks < max_grid ? blocks : max_grid));
     a.wave0 = wave0;
-    if (a.out_prev)
-        hipLaunchKernelGGL((extract_kernel<F, V, D, true, L>), grid, dim3(kBlock), 0, s, a, first,
+    if (R)   // routing mode: no theta_hat output
+        hipLaunchKernelGGL((extract_kernel<F, V, D, false, L, R>), grid, dim3(kBlock), 0, s, a, first,
                            last);
+    else if (a.out_prev)
+        hipLaunchKernelGGL((extract_kernel<F, V, D, true, L, false>), grid, dim3(kBlock), 0, s, a,
+                           first, last);
     else
-        hipLaunchKernelGGL((extract_kernel<F, V, D, false, L>), grid, dim3(kBlock), 0, s, a, first,
-                           last);
+        hipLaunchKernelGGL((extract_kernel<F, V, D, false, L, false>), grid, dim3(kBlock), 0, s, a,
+                           first, last);
     return (int32_t)grid.x * kWaves;
 }
 
-template <bool D, bool L>
+template <bool D, bool L, bool R>
 int32_t launch_all(const ExtractParams& a, bool vec, int64_t max_grid, hipStream_t s)
 {
     const int64_t full = a.n / kWaveTile;
     const int64_t ntiles = (a.n + kWaveTile - 1) / kWaveTile;
     if (vec) {
-        const int32_t w = launch_tiles<true, true, D, L>(a, 0, full, max_grid, 0, s);  // unguarded
-        return w + launch_tiles<false, true, D, L>(a, full, ntiles, max_grid, w, s);   // ragged tail
+        const int32_t w = launch_tiles<true, true, D, L, R>(a, 0, full, max_grid, 0, s);  // unguarded
+        return w + launch_tiles<false, true, D, L, R>(a, full, ntiles, max_grid, w, s);   // ragged
     }
-    return launch_tiles<false, false, D, L>(a, 0, ntiles, max_grid, 0, s);           // scalar loads
+    return launch_tiles<false, false, D, L, R>(a, 0, ntiles, max_grid, 0, s);           // scalar loads
 }
 
 // ---- ordered mode: runs to ascending positions ----------------------------
@@ -592,12 +637,21 @@ hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream, i
     const bool vec = aligned16(a.p) && aligned16(a.m) && aligned16(a.v) &&
                      (a.out_prev == nullptr || aligned16(a.out_prev));
     int32_t w;
-    if (a.literal)
-        w = (a.decay == 1.0f) ? launch_all<true, true>(a, vec, max_grid, stream)
-                              : launch_all<false, true>(a, vec, max_grid, stream);
-    else
-        w = (a.decay == 1.0f) ? launch_all<true, false>(a, vec, max_grid, stream)
-                              : launch_all<false, false>(a, vec, max_grid, stream);
+    const bool one = a.decay == 1.0f;
+    if (a.route) {
+        if (a.literal)
+            w = one ? launch_all<true, true, true>(a, vec, max_grid, stream)
+                    : launch_all<false, true, true>(a, vec, max_grid, stream);
+        else
+            w = one ? launch_all<true, false, true>(a, vec, max_grid, stream)
+                    : launch_all<false, false, true>(a, vec, max_grid, stream);
+    } else if (a.literal) {
+        w = one ? launch_all<true, true, false>(a, vec, max_grid, stream)
+                : launch_all<false, true, false>(a, vec, max_grid, stream);
+    } else {
+        w = one ? launch_all<true, false, false>(a, vec, max_grid, stream)
+                : launch_all<false, false, false>(a, vec, max_grid, stream);
+    }
     if (waves) *waves = w;
     return hipGetLastError();
 }

@@ -26,9 +26,12 @@
 #include <hip/hip_runtime.h>
 
 #include "dte_internal.h"
+#include "route.h"
 
 namespace dte {
 namespace {
+
+using namespace rt;
 
 constexpr int kBlock = 256;
 constexpr int kBlocksPerCU = 8;
@@ -39,130 +42,9 @@ __global__ void zero_i64_kernel(int64_t* p, int64_t n)
     if (i < n) p[i] = 0;
 }
 
-// Receiver offset of coordinate u under op o, or -1 when u is outside o.
-__device__ __forceinline__ int64_t route(const DevOp& o, const uint32_t* u)
-{
-    int64_t j = 0;
-#pragma unroll
-    for (int d = 0; d < DTE_MAX_DIMS; ++d) {
-        if (d < o.ndim) {
-            const uint32_t rel = u[d] - o.src_origin[d];    // wraps when u < a_s
-            if (rel >= o.extent[d]) return -1;
-            j = j * (int64_t)o.dst_shape[d] + (int64_t)(rel + o.dst_origin[d]);
-        }
-    }
-    return o.dst_base + j;
-}
-
 constexpr int kWaves = kBlock / 64;
 constexpr int kRemapSlots = 8;                     // entries per lane per chunk
 constexpr int kChunk = 64 * kRemapSlots;           // entries per wave per chunk
-
-__device__ __forceinline__ int lane_prefix(uint64_t mask)
-{
-    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-}
-
-// Unravel a segment-local offset over a row-major shape of nd dimensions.
-__device__ __forceinline__ void unravel(uint32_t li, int nd, const uint32_t* shape,
-                                        uint32_t* u)
-{
-#pragma unroll
-    for (int d = DTE_MAX_DIMS - 1; d >= 0; --d) {
-        if (d < nd) {
-            if (d == 0) {
-                u[0] = li;
-            } else {
-                const uint32_t q = li / shape[d];
-                u[d] = li - q * shape[d];
-                li = q;
-            }
-        } else {
-            u[d] = 0;
-        }
-    }
-}
-
-__device__ __forceinline__ int64_t readlane64(int64_t x, int lane)
-{
-    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, lane);
-    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)((uint64_t)x >> 32), lane);
-    return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-// Wave-uniform description of the current segment (scalar registers).
-struct SegInfo {
-    int64_t lo, hi;      // flat range [lo, hi); empty before the first lookup
-    int32_t seg, k0, k1; // operations [k0, k1)
-};
-
-// Segment holding the uniform flat offset i0 (0 <= i0 < total).
-__device__ __forceinline__ SegInfo find_segment(const PlanView& pl, int64_t i0)
-{
-    int32_t s = __builtin_amdgcn_readfirstlane(pl.lookup[i0 >> pl.shift]);
-    while (readlane64(pl.seg_begin[s + 1], 0) <= i0) ++s;
-    return SegInfo{readlane64(pl.seg_begin[s], 0), readlane64(pl.seg_begin[s + 1], 0), s,
-                   __builtin_amdgcn_readfirstlane(pl.seg_ops[s]),
-                   __builtin_amdgcn_readfirstlane(pl.seg_ops[s + 1])};
-}
-
-// One operation with every field made wave-uniform (scalar registers).
-__device__ __forceinline__ DevOp load_op(const DevOp* ops, int32_t k)
-{
-    const uint32_t* w = reinterpret_cast<const uint32_t*>(ops + k);
-    DevOp o;
-    uint32_t* d = reinterpret_cast<uint32_t*>(&o);
-#pragma unroll
-    for (int i = 0; i < (int)(sizeof(DevOp) / 4); ++i) d[i] = __builtin_amdgcn_readfirstlane(w[i]);
-    return o;
-}
-
-__device__ __forceinline__ void unravel_in(const PlanView& pl, int32_t s, uint32_t li, uint32_t* u)
-{
-    unravel(li, __builtin_amdgcn_readfirstlane(pl.seg_ndim[s]),
-            pl.seg_shape + (int64_t)s * DTE_MAX_DIMS, u);
-}
-
-// Route one slot lane by lane in groups sharing a segment (used when a
-// chunk spans several segments).  Counters: lane r of `runv` holds the
-// running count of rank first + r, lane r of `basev` the reserved bucket
-// start.  kWrite == false counts outputs; kWrite == true writes them.
-template <bool kWrite>
-__device__ __forceinline__ void route_slot(const PlanView& pl, const RankSlice& out, int lane,
-                                           int64_t i, uint16_t v, int& runv, int64_t basev,
-                                           SegInfo& cache)
-{
-    bool pending = i >= 0;
-    uint64_t pmask = __ballot(pending);
-    while (pmask != 0) {
-        const int src = __builtin_ctzll(pmask);
-        const int64_t i0 = readlane64(i, src);
-        if (!(i0 >= cache.lo && i0 < cache.hi)) cache = find_segment(pl, i0);
-        const bool mine = pending && i >= cache.lo && i < cache.hi;
-        pending = pending && !mine;
-        pmask = __ballot(pending);
-        uint32_t u[DTE_MAX_DIMS];
-        unravel_in(pl, cache.seg, (uint32_t)(i - cache.lo), u);
-        for (int32_t k = cache.k0; k < cache.k1; ++k) {
-            const DevOp o = load_op(pl.ops, k);
-            const int r = o.rank - out.first;
-            if (r < 0 || r >= out.count) continue;
-            const int64_t j = mine ? route(o, u) : -1;
-            const uint64_t b = __ballot(j >= 0);
-            if (b == 0) continue;
-            const int start = __builtin_amdgcn_readlane(runv, r);
-            if (lane == r) runv += __popcll(b);
-            if (kWrite && j >= 0) {
-                const int64_t pos = readlane64(basev, r) + start + lane_prefix(b);
-                if (pos < out.cap[r]) {
-                    out.off[r][pos] = j;
-                    out.val[r][pos] = v;
-                }
-            }
-        }
-    }
-}
 
 // Whole chunk inside one segment: each operation is loaded once and tested
 // against all slots (coordinates kept in registers).

@@ -110,6 +110,28 @@ class DeltaPipeline:
                          out_prev=out_prev[b:e] if out_prev is not None else None,
                          stream=stream)
 
+    def extract_remap(self, p, m, v, hp, n=None, index_base=0, stream=None):
+        """Changed entries routed straight into the buckets (adds to
+        rank_count and to the cursor; clear both first, see step_fused)."""
+        n = p.numel() if n is None else n
+        B.dte_extract_remap(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, index_base, hp,
+                            self.plan.handle, [t.data_ptr() for t in self.off],
+                            [t.data_ptr() for t in self.rval], self.rank_capacity,
+                            self.rank_count.data_ptr(), self.cursor.data_ptr(), _stream(stream))
+
+    def step_fused(self, p, m, v, hp, stream=None, runs=None):
+        """The step with detection and remap in one kernel, then apply."""
+        with torch.cuda.stream(stream) if stream is not None else _null():
+            self.cursor.zero_()
+            self.rank_count.zero_()
+        if runs is None:
+            self.extract_remap(p, m, v, hp, stream=stream)
+        else:
+            for b, e, h in runs:
+                self.extract_remap(p[b:e], m[b:e], v[b:e], h, n=e - b, index_base=b,
+                                   stream=stream)
+        self.apply(stream)
+
     def step(self, p, m, v, hp, stream=None, runs=None):
         """reset, extract (over `runs` when the shard has several parameter
         groups), remap, apply."""

@@ -193,6 +193,23 @@ def test_qwen3_8b_store_round_trip_full(qwen3_8b, tmp_path):
     torch.cuda.empty_cache()
 
 
+def test_qwen3_8b_fused_extract_remap_full(qwen3_8b):
+    """dte_extract_remap at full size: buckets and applied shards equal the
+    oracle's remap of its complete delta."""
+    wl, res, p, m, v = qwen3_8b
+    spec = layouts.build_spec(wl)
+    pl = oplan.build_plan(wl)
+    pipe = DeltaPipeline(spec, capacity=1, rank_capacity=[int(wl.numel * 0.006)] * 4,
+                         shards=sentinel_shards(spec))
+    pipe.step_fused(p, m, v, wl.hp)
+    sync()
+    assert int(pipe.cursor.item()) == res.idx.size
+    check_buckets_and_shards(pipe, pl, oremap.remap(pl, res.idx, res.val))
+    pipe.close()
+    del pipe
+    torch.cuda.empty_cache()
+
+
 def test_qwen3_8b_tp8_apply_full(qwen3_8b):
     """The Qwen3-8B delta remapped to eight TP=8 receivers and applied."""
     wl, res, p, m, v = qwen3_8b

@@ -18,7 +18,7 @@ from oracle import remap as oremap
 from oracle import run as orun
 from paper_2608_00455_amd import binding as B
 from paper_2608_00455_amd import layouts
-from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state
+from paper_2608_00455_amd.pipeline import DeltaPipeline, generate_state, group_runs
 from synth import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -457,3 +457,61 @@ def test_literal_order_at_the_proof_guards(eps):
         assert total == want_idx.size, lr
         assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val), lr
         pipe.close()
+
+
+@pytest.mark.parametrize("make,order", [
+    (lambda: W.scaled_dense(layers=2, tp=2, lr=1e-6), W.ORDER_FOLDED),
+    (lambda: W.scaled_dense(layers=2, tp=2, lr=1e-4), W.ORDER_FOLDED),
+    (lambda: W.scaled_dense(layers=2, tp=2, lr=1e-4), W.ORDER_LITERAL),
+    (lambda: W.tiny_block(), W.ORDER_FOLDED),
+    (lambda: W.scaled_moe(synth.word, layers=2, ranks=8, attn_tp=2, experts=16, hidden=64,
+                          head_dim=16, expert_intermediate=24, lr=1e-5), W.ORDER_FOLDED),
+    (lambda: W.scaled_mcore(trainer_rank=1, receiver_tp=4, vocab=64, lr=1e-5), W.ORDER_FOLDED),
+])
+def test_fused_extract_remap_equals_oracle(make, order):
+    """dte_extract_remap: the buckets (and after apply, the shards) equal the
+    oracle's remap of its delta; the changed count equals the delta size."""
+    wl = make()
+    hp = W.StepHP(lr=wl.hp.lr, order=order)
+    say("case: fused extract+remap", wl.name, hp.lr, order)
+    if wl.sender.kind == "mcore":
+        from oracle import mcore
+        twin = W.canonical_twin(wl)
+        want_d = mcore.extract(wl, hp)
+        pl = oplan.build_plan(twin)
+        st_res = orun.extract(twin, hp=hp, keep=("ph", "p"))
+    else:
+        twin = wl
+        want_d = orun.extract(wl, hp=hp)
+        pl = oplan.build_plan(wl)
+        st_res = orun.extract(wl, hp=hp, keep=("ph", "p"))
+    p, m, v = generate_state(wl, hp)
+    spec = layouts.build_spec(wl)
+    old = oremap.layout(pl, ocore.bf16(orun.flat(st_res.parts, "ph")))
+    pipe = DeltaPipeline(spec, capacity=1, rank_capacity=[max(1, n) for n in spec.rank_numel],
+                         shards=[dev(x.view(np.int16)) for x in old])
+    pipe.step_fused(p, m, v, hp, runs=group_runs(wl, hp))
+    sync()
+    assert int(pipe.cursor.item()) == want_d.idx.size
+    buckets, counts = pipe.buckets()
+    want = oremap.remap(pl, want_d.idx, want_d.val)
+    expect = oremap.apply([x.copy() for x in old], want)
+    for r in range(pl.nranks):
+        assert counts[r] == want[r][0].size, r
+        assert np.array_equal(buckets[r][0], want[r][0]), r
+        assert np.array_equal(buckets[r][1], want[r][1]), r
+        assert np.array_equal(host_u16(pipe.shards[r]), expect[r]), r
+    pipe.close()
+
+
+def test_fused_extract_remap_rejects_plans_over_16_ranks():
+    wl = W.scaled_dense(layers=1, tp=32, heads_q=32, heads_kv=32, head_dim=8, hidden=64,
+                        intermediate=128, vocab=64)
+    say("case: fused rejects 32 ranks")
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=16)
+    p = torch.zeros(wl.numel, dtype=torch.float32, device="cuda")
+    with pytest.raises(B.DteError) as e:
+        pipe.extract_remap(p, p, p, wl.hp)
+    assert e.value.status == B.DTE_ERR_ARG
+    pipe.close()

@@ -1354,6 +1354,8 @@ dte_status dte_store_read_device(const char* dir, int64_t version, int64_t base,
     Ring ring(threads + 2, biggest);
     if (!ring.ok()) return DTE_ERR_HIP;
     std::mutex copy_mutex;   // one copier at a time on the stream
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return DTE_ERR_HIP;
     st = read_chunks(dir, m, threads, [&](size_t k, const uint32_t* local, const uint16_t* v) {
         const int64_t at = m.offset[k];
         if (at >= n) return DTE_OK;
@@ -1364,7 +1366,9 @@ dte_status dte_store_read_device(const char* dir, int64_t version, int64_t base,
         dte_status r = DTE_OK;
         {
             std::lock_guard<std::mutex> g(copy_mutex);
-            if (hipMemcpyAsync(loc + at, ring.local(slot), (size_t)c * 4, hipMemcpyHostToDevice, s) !=
+            // pool threads start on device 0: use the caller's device
+            if (hipSetDevice(device) != hipSuccess ||
+                hipMemcpyAsync(loc + at, ring.local(slot), (size_t)c * 4, hipMemcpyHostToDevice, s) !=
                     hipSuccess ||
                 hipMemcpyAsync(val + at, ring.val(slot), (size_t)c * 2, hipMemcpyHostToDevice, s) !=
                     hipSuccess ||

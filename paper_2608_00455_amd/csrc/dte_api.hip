@@ -356,9 +356,8 @@ int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 OrderedWorkspace ordered_layout(int64_t capacity)
 {
     OrderedWorkspace w;
-    // every flush but a wave's last holds more than 768 entries (a flush
-    // happens when at most 256 more would overflow 1024 staged entries)
-    w.max_runs = capacity / 769 + dte::kMaxOrderedWaves + 1;
+    // every flush but a wave's last holds exactly 1024 entries
+    w.max_runs = capacity / 1024 + dte::kMaxOrderedWaves + 1;
     w.idx = 0;
     w.val = align256(w.idx + capacity * (int64_t)sizeof(int64_t));
     w.runs = align256(w.val + capacity * (int64_t)sizeof(uint16_t));

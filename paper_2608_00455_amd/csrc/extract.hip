@@ -30,8 +30,10 @@
 //    candidates are queued, and changed entries (packed 32-bit position +
 //    BF16 value) staged in LDS, in ascending element order: every wave's
 //    output is ascending.  A wave reserves global output space with one
-//    atomicAdd on the 64-bit cursor per flush of its staging area (1024
-//    entries), then writes the entries out coalesced.  No block-wide barrier anywhere; the number of
+//    atomicAdd on the 64-bit cursor per flush of its staging area, always
+//    exactly 1024 entries except a wave's last flush (so the output is made
+//    of whole 1024-entry runs, each ascending, until the waves finish), then
+//    writes the entries out coalesced.  No block-wide barrier anywhere; the number of
 //    atomics is bounded by entries / 1024 + waves;
 //  - ordered mode: each flush also records (unordered position, entries of
 //    the wave before it, count, wave) and each wave its total; a scan of the
@@ -312,13 +314,25 @@ __device__ __forceinline__ void stage_changed(const ExtractParams& a, const Wave
     const uint64_t k = __ballot(changed);
     if (k == 0) return;
     const int cnt = __popcll(k);
-    if (so.staged + cnt > kWaveStage) flush_wave<kRoute>(a, st, so, lane);
-    if (changed) {
-        const int pos = so.staged + lane_prefix(k);
+    const int before = so.staged;
+    const int pos = before + lane_prefix(k);
+    if (changed && pos < kWaveStage) {
         st.key[pos] = key;
         st.val[pos] = val;
     }
-    so.staged += cnt;
+    if (before + cnt < kWaveStage) {
+        so.staged = before + cnt;
+        return;
+    }
+    // the staging area is full: flush exactly kWaveStage entries (so every
+    // flush but a wave's last is one full, aligned block), then stage the rest
+    so.staged = kWaveStage;
+    flush_wave<kRoute>(a, st, so, lane);
+    if (changed && pos >= kWaveStage) {
+        st.key[pos - kWaveStage] = key;
+        st.val[pos - kWaveStage] = val;
+    }
+    so.staged = before + cnt - kWaveStage;
 }
 
 // Exact inverse of every queued candidate, 64 per pass; changed ones are
@@ -397,18 +411,37 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
             }
             const Slot4 r = select4(sel);
             if (r.count != 0) {
-                if (so.staged + r.count > kWaveStage) flush_wave<kRoute>(a, st, so, lane);
-                const int base = so.staged + lanes_before(r);
+                const int before = so.staged;
+                const int base = before + lanes_before(r);
                 int k = 0;
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     if (sel[c]) {
-                        st.key[base + k] = key0 + c;
-                        st.val[base + k] = (uint16_t)bn[c];
+                        if (base + k < kWaveStage) {
+                            st.key[base + k] = key0 + c;
+                            st.val[base + k] = (uint16_t)bn[c];
+                        }
                         ++k;
                     }
                 }
-                so.staged += r.count;
+                if (before + r.count < kWaveStage) {
+                    so.staged = before + r.count;
+                } else {   // full: flush one whole block, then stage the rest
+                    so.staged = kWaveStage;
+                    flush_wave<kRoute>(a, st, so, lane);
+                    k = 0;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        if (sel[c]) {
+                            if (base + k >= kWaveStage) {
+                                st.key[base + k - kWaveStage] = key0 + c;
+                                st.val[base + k - kWaveStage] = (uint16_t)bn[c];
+                            }
+                            ++k;
+                        }
+                    }
+                    so.staged = before + r.count - kWaveStage;
+                }
             }
             if (kFull || (kVecLoads && off + 3 < rem)) {
                 __builtin_nontemporal_store(prev, reinterpret_cast<f32x4*>(a.out_prev + t0 + off));

@@ -127,8 +127,8 @@ __device__ __forceinline__ void route_range(const PlanView& pl, const RankSlice&
 }
 
 // Block b owns entries [total b / G, total (b+1) / G), both ends rounded
-// down to whole chunks (the last block ends at total); its waves take every
-// fourth chunk.  Pass 1 counts per rank, the block reserves bucket space
+// down to whole chunks when the delta has at least four chunks per block
+// (the last block ends at total); its waves take every fourth chunk.  Pass 1 counts per rank, the block reserves bucket space
 // with one atomicAdd per rank, pass 2 writes: wave w of the block writes
 // after the outputs of waves 0..w-1, each wave in its own chunk order.
 __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_t* __restrict__ idx,
@@ -145,12 +145,13 @@ __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_
     if (total < 0) total = 0;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    // slices start on chunk boundaries: extract flushes whole 1024-entry
-    // runs, so a chunk then lies in one run (usually one segment)
-    const int64_t lo = total * blockIdx.x / gridDim.x / kChunk * kChunk;
-    const int64_t hi = blockIdx.x + 1 == gridDim.x
-                           ? total
-                           : total * (blockIdx.x + 1) / gridDim.x / kChunk * kChunk;
+    // slices start on chunk boundaries when each block gets several chunks:
+    // extract flushes whole 1024-entry runs, so a chunk then lies in one run
+    // (usually one segment); small deltas are split evenly instead
+    const int64_t g = gridDim.x;
+    const int64_t align = total >= g * 4 * kChunk ? kChunk : 1;
+    const int64_t lo = total * blockIdx.x / g / align * align;
+    const int64_t hi = blockIdx.x + 1 == g ? total : total * (blockIdx.x + 1) / g / align * align;
     SegInfo cache{0, 0, 0, 0, 0};
 
     int runv = 0;                                       // lane r: outputs for rank first + r

@@ -210,7 +210,7 @@ def main():
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU; the multi-GPU exchange is not implemented "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         return 2
 

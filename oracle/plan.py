@@ -5,8 +5,8 @@ parameter p and receiver r, the hyperrectangular overlap between the
 sender's canonical tensor view (shape n_s) and the receiver-local shard
 (shape n_r), given by the origins a_s, a_r and the extent e.
 
-The receiver layouts are this build's reading of the inference engine's
-sharding (the paper gives only the fused-QKV example of appendix B):
+The receiver layouts are a reading of the inference engine's sharding (the
+paper gives only the fused-QKV example of appendix B):
   dense TP=P: qkv_proj = [q_r; k_r; v_r], gate_up_proj = [gate_r; up_r]
   (row slices), o_proj and down_proj split along their input columns,
   embed_tokens and lm_head split by vocabulary rows, norms replicated;

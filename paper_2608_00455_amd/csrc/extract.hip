@@ -207,7 +207,7 @@ __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging&
     if (kRoute) {
         if (lane == 0)
             atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor), (unsigned long long)staged);
-        rt::SegInfo cache{0, 0, 0, 0, 0};
+        rt::SegInfo cache{};
         int runv = 0;                            // lane r: entries for rank out.first + r
 #pragma unroll 1
         for (int pass = 0; pass < 2; ++pass) {

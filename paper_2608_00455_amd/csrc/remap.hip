@@ -34,7 +34,6 @@ namespace {
 using namespace rt;
 
 constexpr int kBlock = 256;
-constexpr int kBlocksPerCU = 8;
 
 __global__ void zero_i64_kernel(int64_t* p, int64_t n)
 {
@@ -45,10 +44,23 @@ __global__ void zero_i64_kernel(int64_t* p, int64_t n)
 constexpr int kWaves = kBlock / 64;
 constexpr int kRemapSlots = 8;                     // entries per lane per chunk
 constexpr int kChunk = 64 * kRemapSlots;           // entries per wave per chunk
+// Slice size and grid of remap: many small slices balance the uneven cost
+// of routing (segments differ in operation count) better than one slice
+// per resident block, but every block costs a reservation round trip, so a
+// block takes about kBlockEntries entries, or fewer (down to
+// kMinBlockEntries) while that leaves CUs idle.  The count is on the
+// device: the grid is sized for the capacity and surplus blocks leave at
+// once.
+constexpr int64_t kBlockEntries = 4096;
+constexpr int64_t kMinBlockEntries = 1024;
+constexpr int kRemapBlocksPerCU = 64;
+constexpr int kRemapFillPerCU = 5;                 // blocks per CU that keep the chip busy
 
-// Whole chunk inside one segment: each operation is loaded once and tested
-// against all slots (coordinates kept in registers).
-template <bool kWrite>
+// Whole chunk inside one segment of kNd dimensions: each
+// operation is loaded once (scalar registers) and tested against all slots,
+// whose coordinates stay in registers.  The counting pass only tests
+// containment; the writing pass ravels the contained coordinates.
+template <bool kWrite, int kNd>
 __device__ __forceinline__ void route_chunk(const PlanView& pl, const RankSlice& out, int lane,
                                             const SegInfo& sg, const int64_t* x, const uint16_t* y,
                                             const uint32_t (*u)[DTE_MAX_DIMS], int& runv,
@@ -59,22 +71,36 @@ __device__ __forceinline__ void route_chunk(const PlanView& pl, const RankSlice&
         const int r = o.rank - out.first;
         if (r < 0 || r >= out.count) continue;
         int run = __builtin_amdgcn_readlane(runv, r);
+        int64_t* const off = out.off[r];
+        uint16_t* const val = out.val[r];
+        const int64_t cap = out.cap[r];
         const int64_t base = kWrite ? readlane64(basev, r) : 0;
 #pragma unroll
         for (int j = 0; j < kRemapSlots; ++j) {
-            const int64_t t = x[j] >= 0 ? route(o, u[j]) : -1;
-            const uint64_t b = __ballot(t >= 0);
-            if (kWrite && t >= 0) {
+            const bool in = x[j] >= 0 && inside<kNd>(o, u[j]);
+            const uint64_t b = __ballot(in);
+            if (kWrite && in) {
                 const int64_t pos = base + run + lane_prefix(b);
-                if (pos < out.cap[r]) {
-                    out.off[r][pos] = t;
-                    out.val[r][pos] = y[j];
+                if (pos < cap) {
+                    off[pos] = ravel<kNd>(o, u[j]);
+                    val[pos] = y[j];
                 }
             }
             run += __popcll(b);
         }
         if (lane == r) runv = run;
     }
+}
+
+template <bool kWrite, int kNd>
+__device__ __forceinline__ void route_chunk_in(const PlanView& pl, const RankSlice& out, int lane,
+                                               const SegInfo& sg, const int64_t* x,
+                                               const uint16_t* y, int& runv, int64_t basev)
+{
+    uint32_t u[kRemapSlots][DTE_MAX_DIMS];
+#pragma unroll
+    for (int j = 0; j < kRemapSlots; ++j) unravel<kNd>((uint32_t)(x[j] - sg.lo), sg, u[j]);
+    route_chunk<kWrite, kNd>(pl, out, lane, sg, x, y, u, runv, basev);
 }
 
 // Route the chunk of entries [c0, c1): counting pass (kWrite == false) or
@@ -113,12 +139,12 @@ __device__ __forceinline__ void route_range(const PlanView& pl, const RankSlice&
 #pragma unroll
     for (int j = 0; j < kRemapSlots; ++j)
         inside = inside && (x[j] < 0 || (x[j] >= cache.lo && x[j] < cache.hi));
-    if (__ballot(!inside) == 0) {
-        uint32_t u[kRemapSlots][DTE_MAX_DIMS];
-#pragma unroll
-        for (int j = 0; j < kRemapSlots; ++j)
-            unravel_in(pl, cache.seg, (uint32_t)(x[j] - cache.lo), u[j]);
-        route_chunk<kWrite>(pl, out, lane, cache, x, y, u, runv, basev);
+    const bool one = __ballot(!inside) == 0;
+    // matrices and vectors (nearly every segment) get straight-line code
+    if (one && cache.nd == 2) {
+        route_chunk_in<kWrite, 2>(pl, out, lane, cache, x, y, runv, basev);
+    } else if (one && cache.nd == 1) {
+        route_chunk_in<kWrite, 1>(pl, out, lane, cache, x, y, runv, basev);
     } else {
 #pragma unroll 1
         for (int j = 0; j < kRemapSlots; ++j)
@@ -126,16 +152,19 @@ __device__ __forceinline__ void route_range(const PlanView& pl, const RankSlice&
     }
 }
 
-// Block b owns entries [total b / G, total (b+1) / G), both ends rounded
-// down to whole chunks when the delta has at least four chunks per block
-// (the last block ends at total); its waves take every fourth chunk.  Pass 1 counts per rank, the block reserves bucket space
-// with one atomicAdd per rank, pass 2 writes: wave w of the block writes
-// after the outputs of waves 0..w-1, each wave in its own chunk order.
+// G blocks take part (see kBlockEntries).  Block b < G
+// owns entries [total b / G, total (b+1) / G), both ends rounded down to
+// whole chunks when the delta has at least four chunks per block (the last
+// block ends at total); its waves take every fourth chunk.  Pass 1 counts
+// per rank, the block reserves bucket space with one atomicAdd per rank,
+// pass 2 writes: wave w of the block writes after the outputs of waves
+// 0..w-1, each wave in its own chunk order.
 __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_t* __restrict__ idx,
                                                        const uint16_t* __restrict__ val,
                                                        const int64_t* __restrict__ count,
                                                        int64_t in_capacity, RankSlice out,
-                                                       int64_t* __restrict__ rank_count)
+                                                       int64_t* __restrict__ rank_count,
+                                                       int64_t fill)
 {
     __shared__ int s_cnt[kWaves][kRanksPerLaunch];
     __shared__ int64_t s_base[kRanksPerLaunch];
@@ -148,11 +177,18 @@ __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_
     // slices start on chunk boundaries when each block gets several chunks:
     // extract flushes whole 1024-entry runs, so a chunk then lies in one run
     // (usually one segment); small deltas are split evenly instead
-    const int64_t g = gridDim.x;
+    // blocks in use: about kBlockEntries entries each, more (at least
+    // kMinBlockEntries each) up to `fill` blocks, at most the grid
+    int64_t g = (total + kBlockEntries - 1) / kBlockEntries;
+    const int64_t gmin = (total + kMinBlockEntries - 1) / kMinBlockEntries;
+    const int64_t gfill = gmin < fill ? gmin : fill;
+    g = g > gfill ? g : gfill;
+    g = g < 1 ? 1 : (g > (int64_t)gridDim.x ? (int64_t)gridDim.x : g);
+    if ((int64_t)blockIdx.x >= g) return;
     const int64_t align = total >= g * 4 * kChunk ? kChunk : 1;
     const int64_t lo = total * blockIdx.x / g / align * align;
     const int64_t hi = blockIdx.x + 1 == g ? total : total * (blockIdx.x + 1) / g / align * align;
-    SegInfo cache{0, 0, 0, 0, 0};
+    SegInfo cache{};
 
     int runv = 0;                                       // lane r: outputs for rank first + r
     for (int64_t c0 = lo + (int64_t)wave * kChunk; c0 < hi; c0 += (int64_t)kWaves * kChunk)
@@ -211,6 +247,19 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(ApplySlice s,
     }
 }
 
+// Blocks of `kernel` that fit on one CU at once (register- and LDS-bound),
+// so that a grid of cus * resident blocks runs in a single round: a grid of
+// equal slices that needs a second, partial round of blocks leaves most of
+// the chip idle during that round.
+template <typename Kernel>
+int resident_blocks(Kernel kernel)
+{
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, kBlock, 0) != hipSuccess || n < 1)
+        n = 1;
+    return n;
+}
+
 }  // namespace
 
 hipError_t launch_zero_i64(int64_t* p, int64_t n, hipStream_t stream)
@@ -226,16 +275,19 @@ hipError_t launch_remap(const PlanView& plan, const int64_t* idx, const uint16_t
                         int64_t* rank_count, int cus, hipStream_t stream)
 {
     if (in_capacity <= 0) return hipSuccess;
-    const dim3 grid((unsigned)cus * kBlocksPerCU);     // persistent: the count is on the device
+    int64_t blocks = (in_capacity + kBlockEntries - 1) / kBlockEntries;
+    if (blocks > (int64_t)cus * kRemapBlocksPerCU) blocks = (int64_t)cus * kRemapBlocksPerCU;
+    const dim3 grid((unsigned)blocks);
     hipLaunchKernelGGL(remap_kernel, grid, dim3(kBlock), 0, stream, plan, idx, val, count,
-                       in_capacity, out, rank_count);
+                       in_capacity, out, rank_count, (int64_t)cus * kRemapFillPerCU);
     return hipGetLastError();
 }
 
 hipError_t launch_apply(const ApplySlice& s, const int64_t* rank_count, int cus,
                         hipStream_t stream)
 {
-    const dim3 grid((unsigned)cus * 8);
+    static const int per_cu = resident_blocks(apply_kernel);
+    const dim3 grid((unsigned)(cus * per_cu));
     hipLaunchKernelGGL(apply_kernel, grid, dim3(kBlock), 0, stream, s, rank_count);
     return hipGetLastError();
 }

@@ -18,39 +18,30 @@ __device__ __forceinline__ int lane_prefix(uint64_t mask)
                                           __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-// Receiver offset of coordinate u under op o, or -1 when u is outside o.
-__device__ __forceinline__ int64_t route(const DevOp& o, const uint32_t* u)
+// Containment a_s <= u < a_s + e of coordinate u in operation o, without
+// branches (u < a_s wraps to a large value).  kNd > 0: the segment's
+// dimension count, known at compile time; kNd == 0: o.ndim (wave-uniform).
+template <int kNd>
+__device__ __forceinline__ bool inside(const DevOp& o, const uint32_t* u)
 {
-    int64_t j = 0;
+    bool in = true;
 #pragma unroll
-    for (int d = 0; d < DTE_MAX_DIMS; ++d) {
-        if (d < o.ndim) {
-            const uint32_t rel = u[d] - o.src_origin[d];    // wraps when u < a_s
-            if (rel >= o.extent[d]) return -1;
-            j = j * (int64_t)o.dst_shape[d] + (int64_t)(rel + o.dst_origin[d]);
-        }
-    }
-    return o.dst_base + j;
+    for (int d = 0; d < DTE_MAX_DIMS; ++d)
+        if (kNd > 0 ? d < kNd : d < o.ndim) in = in & (u[d] - o.src_origin[d] < o.extent[d]);
+    return in;
 }
 
-// Unravel a segment-local offset over a row-major shape of nd dimensions.
-__device__ __forceinline__ void unravel(uint32_t li, int nd, const uint32_t* shape,
-                                        uint32_t* u)
+// Receiver offset of a contained coordinate: u - a_s + a_r raveled over the
+// receiver view n_r, plus the view's base (eq. receiver_local_remapping).
+template <int kNd>
+__device__ __forceinline__ int64_t ravel(const DevOp& o, const uint32_t* u)
 {
+    uint64_t j = 0;
 #pragma unroll
-    for (int d = DTE_MAX_DIMS - 1; d >= 0; --d) {
-        if (d < nd) {
-            if (d == 0) {
-                u[0] = li;
-            } else {
-                const uint32_t q = li / shape[d];
-                u[d] = li - q * shape[d];
-                li = q;
-            }
-        } else {
-            u[d] = 0;
-        }
-    }
+    for (int d = 0; d < DTE_MAX_DIMS; ++d)
+        if (kNd > 0 ? d < kNd : d < o.ndim)
+            j = j * o.dst_shape[d] + (uint32_t)(u[d] - o.src_origin[d] + o.dst_origin[d]);
+    return o.dst_base + (int64_t)j;
 }
 
 __device__ __forceinline__ int64_t readlane64(int64_t x, int lane)
@@ -64,6 +55,8 @@ __device__ __forceinline__ int64_t readlane64(int64_t x, int lane)
 struct SegInfo {
     int64_t lo, hi;      // flat range [lo, hi); empty before the first lookup
     int32_t seg, k0, k1; // operations [k0, k1)
+    int32_t nd;          // dimensions of the segment's shape
+    uint32_t shape[DTE_MAX_DIMS];
 };
 
 // Segment holding the uniform flat offset i0 (0 <= i0 < total).
@@ -71,9 +64,17 @@ __device__ __forceinline__ SegInfo find_segment(const PlanView& pl, int64_t i0)
 {
     int32_t s = __builtin_amdgcn_readfirstlane(pl.lookup[i0 >> pl.shift]);
     while (readlane64(pl.seg_begin[s + 1], 0) <= i0) ++s;
-    return SegInfo{readlane64(pl.seg_begin[s], 0), readlane64(pl.seg_begin[s + 1], 0), s,
-                   __builtin_amdgcn_readfirstlane(pl.seg_ops[s]),
-                   __builtin_amdgcn_readfirstlane(pl.seg_ops[s + 1])};
+    SegInfo g;
+    g.lo = readlane64(pl.seg_begin[s], 0);
+    g.hi = readlane64(pl.seg_begin[s + 1], 0);
+    g.seg = s;
+    g.k0 = __builtin_amdgcn_readfirstlane(pl.seg_ops[s]);
+    g.k1 = __builtin_amdgcn_readfirstlane(pl.seg_ops[s + 1]);
+    g.nd = __builtin_amdgcn_readfirstlane(pl.seg_ndim[s]);
+#pragma unroll
+    for (int d = 0; d < DTE_MAX_DIMS; ++d)
+        g.shape[d] = __builtin_amdgcn_readfirstlane(pl.seg_shape[(int64_t)s * DTE_MAX_DIMS + d]);
+    return g;
 }
 
 // One operation with every field made wave-uniform (scalar registers).
@@ -87,10 +88,25 @@ __device__ __forceinline__ DevOp load_op(const DevOp* ops, int32_t k)
     return o;
 }
 
-__device__ __forceinline__ void unravel_in(const PlanView& pl, int32_t s, uint32_t li, uint32_t* u)
+// Unravel a segment-local offset over the segment's row-major shape
+// (eq. canonical_unravel); kNd as for `inside` (kNd == 0: g.nd).
+template <int kNd>
+__device__ __forceinline__ void unravel(uint32_t li, const SegInfo& g, uint32_t* u)
 {
-    unravel(li, __builtin_amdgcn_readfirstlane(pl.seg_ndim[s]),
-            pl.seg_shape + (int64_t)s * DTE_MAX_DIMS, u);
+#pragma unroll
+    for (int d = DTE_MAX_DIMS - 1; d >= 0; --d) {
+        if (kNd > 0 ? d < kNd : d < g.nd) {
+            if (d == 0) {
+                u[0] = li;
+            } else {
+                const uint32_t q = li / g.shape[d];
+                u[d] = li - q * g.shape[d];
+                li = q;
+            }
+        } else {
+            u[d] = 0;
+        }
+    }
 }
 
 // Route one slot lane by lane in groups sharing a segment (used when a
@@ -112,21 +128,24 @@ __device__ __forceinline__ void route_slot(const PlanView& pl, const RankSlice& 
         pending = pending && !mine;
         pmask = __ballot(pending);
         uint32_t u[DTE_MAX_DIMS];
-        unravel_in(pl, cache.seg, (uint32_t)(i - cache.lo), u);
+        unravel<0>((uint32_t)(i - cache.lo), cache, u);
         for (int32_t k = cache.k0; k < cache.k1; ++k) {
             const DevOp o = load_op(pl.ops, k);
             const int r = o.rank - out.first;
             if (r < 0 || r >= out.count) continue;
-            const int64_t j = mine ? route(o, u) : -1;
-            const uint64_t b = __ballot(j >= 0);
+            const bool in = mine && inside<0>(o, u);
+            const uint64_t b = __ballot(in);
             if (b == 0) continue;
             const int start = __builtin_amdgcn_readlane(runv, r);
             if (lane == r) runv += __popcll(b);
-            if (kWrite && j >= 0) {
+            if (kWrite) {
+                int64_t* const off = out.off[r];
+                uint16_t* const val = out.val[r];
+                const int64_t cap = out.cap[r];
                 const int64_t pos = readlane64(basev, r) + start + lane_prefix(b);
-                if (pos < out.cap[r]) {
-                    out.off[r][pos] = j;
-                    out.val[r][pos] = v;
+                if (in && pos < cap) {
+                    off[pos] = ravel<0>(o, u);
+                    val[pos] = v;
                 }
             }
         }

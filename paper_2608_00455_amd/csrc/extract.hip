@@ -232,9 +232,9 @@ __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging&
                     if (x >= a.plan.total) x = -1;
                 }
                 if (pass == 0)
-                    rt::route_slot<false>(a.plan, a.out, lane, x, y, runv, 0, cache);
+                    rt::route_slot<false, false>(a.plan, a.out, lane, x, y, runv, 0, cache);
                 else
-                    rt::route_slot<true>(a.plan, a.out, lane, x, y, runv, basev, cache);
+                    rt::route_slot<true, false>(a.plan, a.out, lane, x, y, runv, basev, cache);
             }
         }
         so.flushed += staged;

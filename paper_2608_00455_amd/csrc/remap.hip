@@ -99,7 +99,7 @@ __device__ __forceinline__ void route_chunk_in(const PlanView& pl, const RankSli
 {
     uint32_t u[kRemapSlots][DTE_MAX_DIMS];
 #pragma unroll
-    for (int j = 0; j < kRemapSlots; ++j) unravel<kNd>((uint32_t)(x[j] - sg.lo), sg, u[j]);
+    for (int j = 0; j < kRemapSlots; ++j) unravel<kNd>((uint32_t)(x[j] - sg.lo), kNd, sg.shape, u[j]);
     route_chunk<kWrite, kNd>(pl, out, lane, sg, x, y, u, runv, basev);
 }
 

@@ -88,19 +88,19 @@ __device__ __forceinline__ DevOp load_op(const DevOp* ops, int32_t k)
     return o;
 }
 
-// Unravel a segment-local offset over the segment's row-major shape
-// (eq. canonical_unravel); kNd as for `inside` (kNd == 0: g.nd).
+// Unravel a segment-local offset over a row-major shape of nd dimensions
+// (eq. canonical_unravel); kNd as for `inside` (kNd == 0: nd).
 template <int kNd>
-__device__ __forceinline__ void unravel(uint32_t li, const SegInfo& g, uint32_t* u)
+__device__ __forceinline__ void unravel(uint32_t li, int nd, const uint32_t* shape, uint32_t* u)
 {
 #pragma unroll
     for (int d = DTE_MAX_DIMS - 1; d >= 0; --d) {
-        if (kNd > 0 ? d < kNd : d < g.nd) {
+        if (kNd > 0 ? d < kNd : d < nd) {
             if (d == 0) {
                 u[0] = li;
             } else {
-                const uint32_t q = li / g.shape[d];
-                u[d] = li - q * g.shape[d];
+                const uint32_t q = li / shape[d];
+                u[d] = li - q * shape[d];
                 li = q;
             }
         } else {
@@ -113,7 +113,9 @@ __device__ __forceinline__ void unravel(uint32_t li, const SegInfo& g, uint32_t*
 // chunk spans several segments).  Counters: lane r of `runv` holds the
 // running count of rank first + r, lane r of `basev` the reserved bucket
 // start.  kWrite == false counts outputs; kWrite == true writes them.
-template <bool kWrite>
+// kShapeRegs: unravel over the shape cached in `cache` (else re-read it,
+// which needs fewer registers).
+template <bool kWrite, bool kShapeRegs = true>
 __device__ __forceinline__ void route_slot(const PlanView& pl, const RankSlice& out, int lane,
                                            int64_t i, uint16_t v, int& runv, int64_t basev,
                                            SegInfo& cache)
@@ -128,7 +130,12 @@ __device__ __forceinline__ void route_slot(const PlanView& pl, const RankSlice& 
         pending = pending && !mine;
         pmask = __ballot(pending);
         uint32_t u[DTE_MAX_DIMS];
-        unravel<0>((uint32_t)(i - cache.lo), cache, u);
+        if (kShapeRegs)
+            unravel<0>((uint32_t)(i - cache.lo), cache.nd, cache.shape, u);
+        else
+            unravel<0>((uint32_t)(i - cache.lo),
+                       __builtin_amdgcn_readfirstlane(pl.seg_ndim[cache.seg]),
+                       pl.seg_shape + (int64_t)cache.seg * DTE_MAX_DIMS, u);
         for (int32_t k = cache.k0; k < cache.k1; ++k) {
             const DevOp o = load_op(pl.ops, k);
             const int r = o.rank - out.first;

@@ -336,6 +336,9 @@ def main():
     else:
         step_bytes = 12 * n + 10 * changed + 10 * changed + 10 * routed + 12 * routed
     achieved = k_bytes / (k_ms / 1e3) / 1e9
+    # the counters were taken for the default configuration only (folded
+    # order, unordered output, one parameter group)
+    default_mode = not (args.ordered or args.fused or args.literal or args.norm_group)
     out = {
         "metric": "delta-extract+remap+apply: elements/s and HBM GB/s (% of peak), "
                   "Qwen3-8B shape",
@@ -359,7 +362,9 @@ def main():
                    "step_frac_of_hbm_peak": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS},
         "roofline": {"kernel": kernel, "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": measured_traffic(wl.name, kernel), "kernel_ms": k_ms,
+                     "traffic": (measured_traffic(wl.name, kernel)
+                                 if default_mode else None),
+                     "kernel_ms": k_ms,
                      "bytes_per_launch": k_bytes},
     }
     if not apply_only:

@@ -7,6 +7,7 @@ FP32 instructions.
 import os
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "csrc")
@@ -35,7 +36,7 @@ def build(extra=()):
 
 def asm(source="extract.hip", out=None):
     """Device assembly of one source, for instruction inspection."""
-    out = out or os.path.join(HERE, "..", "_work", source.replace(".hip", ".s"))
+    out = out or os.path.join(tempfile.gettempdir(), source.replace(".hip", ".s"))
     cmd = [hipcc()] + [f for f in HIPCC_FLAGS if f not in ("-shared", "-fPIC")] + \
         ["--cuda-device-only", "-S", "-o", out, os.path.join(SRC, source)]
     subprocess.check_call(cmd)

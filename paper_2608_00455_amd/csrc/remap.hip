@@ -52,7 +52,7 @@ constexpr int kChunk = 64 * kRemapSlots;           // entries per wave per chunk
 // device: the grid is sized for the capacity and surplus blocks leave at
 // once.
 constexpr int64_t kBlockEntries = 4096;
-constexpr int64_t kMinBlockEntries = 1024;
+constexpr int64_t kMinBlockEntries = 64;
 constexpr int kRemapBlocksPerCU = 64;
 constexpr int kRemapFillPerCU = 5;                 // blocks per CU that keep the chip busy
 
@@ -275,11 +275,16 @@ hipError_t launch_remap(const PlanView& plan, const int64_t* idx, const uint16_t
                         int64_t* rank_count, int cus, hipStream_t stream)
 {
     if (in_capacity <= 0) return hipSuccess;
+    // the most blocks the kernel can use for in_capacity entries (its rule
+    // for G with total = in_capacity)
+    const int64_t fill = (int64_t)cus * kRemapFillPerCU;
     int64_t blocks = (in_capacity + kBlockEntries - 1) / kBlockEntries;
+    const int64_t gmin = (in_capacity + kMinBlockEntries - 1) / kMinBlockEntries;
+    blocks = blocks > (gmin < fill ? gmin : fill) ? blocks : (gmin < fill ? gmin : fill);
     if (blocks > (int64_t)cus * kRemapBlocksPerCU) blocks = (int64_t)cus * kRemapBlocksPerCU;
     const dim3 grid((unsigned)blocks);
     hipLaunchKernelGGL(remap_kernel, grid, dim3(kBlock), 0, stream, plan, idx, val, count,
-                       in_capacity, out, rank_count, (int64_t)cus * kRemapFillPerCU);
+                       in_capacity, out, rank_count, fill);
     return hipGetLastError();
 }
 

@@ -220,3 +220,9 @@ def test_ordered_workspace_and_argument_errors():
                None) == B.DTE_ERR_ARG
     assert ext(16, 16, 16, -1, 0, ctypes.byref(hp), 16, 16, 4, 16, 256, need, None,
                None) == B.DTE_ERR_ARG
+
+
+def test_high_dimensional_plan_passes_validation():
+    from highdim_plan import HighDimSpec
+    spec = HighDimSpec()
+    assert _create_status(spec) in (B.DTE_OK, B.DTE_ERR_HIP)

@@ -71,3 +71,40 @@ def test_real_workload_plan_sizes(make, ranks, rank_numel, nseg, nops):
     assert vol.sum() == sum(pl.rank_numel)
     numel = np.array([t.numel for t in wl.tensors], np.int64)
     assert np.all(vol % numel == 0) and np.all(vol >= numel)
+
+
+def test_oracle_remap_on_one_to_four_dimensional_segments_by_brute_force():
+    """The oracle's remap (numpy unravel / ravel) against coordinates worked
+    out by repeated division and Horner's rule, one element at a time, on a
+    sample of every segment of a plan with 1-D to 4-D segments."""
+    from highdim_plan import HighDimSpec
+    from oracle import remap as oremap
+    spec = HighDimSpec()
+    pl = spec.oracle_plan
+    rng = np.random.default_rng(26080455 + 43)
+    idx = np.unique(np.concatenate([
+        rng.integers(b, b + int(np.prod(s)), 400) for b, s in zip(pl.seg_begin, pl.seg_shape)]))
+    val = (idx % 65521).astype(np.uint16)
+    got = oremap.remap(pl, idx, val)
+    want = [dict() for _ in range(pl.nranks)]
+    for i, x in zip(idx.tolist(), val.tolist()):
+        s = max(k for k, b in enumerate(pl.seg_begin) if b <= i)
+        rest = i - pl.seg_begin[s]
+        shape = pl.seg_shape[s]
+        u = [0] * len(shape)
+        for d in range(len(shape) - 1, -1, -1):
+            rest, u[d] = divmod(rest, shape[d])
+        for o in pl.ops:
+            if o.segment != s:
+                continue
+            if all(o.src_origin[d] <= u[d] < o.src_origin[d] + o.extent[d]
+                   for d in range(len(shape))):
+                j = 0
+                for d in range(len(shape)):
+                    j = j * o.dst_shape[d] + (u[d] - o.src_origin[d] + o.dst_origin[d])
+                assert o.dst_base + j not in want[o.rank]
+                want[o.rank][o.dst_base + j] = x
+    for r in range(pl.nranks):
+        keys = sorted(want[r])
+        assert np.array_equal(got[r][0], np.array(keys, dtype=np.int64))
+        assert np.array_equal(got[r][1], np.array([want[r][k] for k in keys], dtype=np.uint16))

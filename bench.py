@@ -2,9 +2,11 @@
 """Throughput of the delta-extraction hot path on one MI355X.
 
 One step = one pass of the whole path over the trainer shard already
-resident in HBM: reset the delta cursor, dte_extract_delta (AdamW
-inversion + BF16 change detection + compaction), dte_remap (receiver
-coordinates) and dte_apply (scatter into the receiver BF16 shards).
+resident in HBM: reset the delta cursor, dte_extract_delta_ordered (AdamW
+inversion + BF16 change detection + compaction into an ascending delta;
+--unordered: dte_extract_delta, whose runs land in any order), dte_remap
+(receiver coordinates) and dte_apply (scatter into the receiver BF16
+shards).
 
 Default workload: the full Qwen3-8B state (8,190,735,360 fp32 elements of
 theta, m, v; receiver TP=4).  Prints one JSON line with the throughput in
@@ -101,16 +103,18 @@ def cpu_baseline(seconds_target=10.0):
             "seconds": secs}
 
 
-def measured_traffic(workload_name, kernel):
-    """HBM bytes per launch of the dominant kernel from the committed
+def measured_traffic(workload_name, kernel, mode):
+    """HBM bytes per call of the dominant kernel(s) from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE record (scaled by a plain copy's
-    counter reading), or None when there is no record for this workload or
-    the kernel source changed since the counters were taken."""
+    counter reading), or None when there is no record for this workload and
+    mode or the kernel source changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "%s_%s_traffic.json" % (kernel, workload_name))
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
+    if rec.get("mode") != mode:
+        return None
     src = os.path.join(ROOT, rec["kernel_source"])
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["kernel_source_sha256"]:
         return None
@@ -188,8 +192,9 @@ def main():
     ap.add_argument("--fused", action="store_true",
                     help="dte_extract_remap (detection routed straight into the buckets) "
                          "instead of dte_extract_delta + dte_remap")
-    ap.add_argument("--ordered", action="store_true",
-                    help="dte_extract_delta_ordered (ascending, deterministic delta)")
+    ap.add_argument("--unordered", action="store_true",
+                    help="dte_extract_delta (runs of the delta in any order) instead of "
+                         "dte_extract_delta_ordered (ascending, deterministic delta)")
     ap.add_argument("--norm-group", action="store_true",
                     help="norms in a parameter group without weight decay")
     ap.add_argument("--capacity-fraction", type=float, default=None,
@@ -243,7 +248,8 @@ def main():
     if frac is None:
         frac = 0.25 if args.workload == "qwen3_8b_4l_tp4" else 0.02
     cap = max(1 << 20, int(n * frac))
-    pipe = DeltaPipeline(spec, capacity=cap, ordered=args.ordered)
+    ordered = not (args.unordered or args.fused)
+    pipe = DeltaPipeline(spec, capacity=cap, ordered=ordered)
     runs = group_runs(wl, hp)
     stream = torch.cuda.current_stream()
     apply_only = args.workload.endswith("_apply")
@@ -337,8 +343,8 @@ def main():
         step_bytes = 12 * n + 10 * changed + 10 * changed + 10 * routed + 12 * routed
     achieved = k_bytes / (k_ms / 1e3) / 1e9
     # the counters were taken for the default configuration only (folded
-    # order, unordered output, one parameter group)
-    default_mode = not (args.ordered or args.fused or args.literal or args.norm_group)
+    # order, ordered output, one parameter group)
+    default_mode = not (args.unordered or args.fused or args.literal or args.norm_group)
     out = {
         "metric": "delta-extract+remap+apply: elements/s and HBM GB/s (% of peak), "
                   "Qwen3-8B shape",
@@ -354,7 +360,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
         "config": {"workload": wl.name, "elements": n, "changed": changed, "extract_calls": len(runs), "settle_s": args.settle,
-                   "ordered": bool(args.ordered), "fused": bool(args.fused), "order": "literal" if args.literal else "folded",
+                   "ordered": ordered, "fused": bool(args.fused), "order": "literal" if args.literal else "folded",
                    "change_fraction": c, "receiver_ranks": len(counts),
                    "routed_entries": routed, "lr": hp.lr,
                    "step_algorithmic_bytes": step_bytes,
@@ -362,7 +368,7 @@ def main():
                    "step_frac_of_hbm_peak": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS},
         "roofline": {"kernel": kernel, "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": (measured_traffic(wl.name, kernel)
+                     "traffic": (measured_traffic(wl.name, kernel, "ordered")
                                  if default_mode else None),
                      "kernel_ms": k_ms,
                      "bytes_per_launch": k_bytes},

@@ -136,8 +136,8 @@ dte_status dte_extract_delta(const float* p, const float* m, const float* v, int
                              float* out_prev, void* stream);
 
 /* Bytes of device workspace that dte_extract_delta_ordered needs for a
- * given capacity (about 10 bytes per entry of capacity plus a fixed
- * 256 KB); -1 if capacity is negative or above 2^40. */
+ * given capacity (about 20 bytes per entry of capacity plus a fixed
+ * 0.8 MB); -1 if capacity is negative or above 2^40. */
 int64_t dte_ordered_workspace_bytes(int64_t capacity);
 
 /* dte_extract_delta with the entries in ascending offset order (paper

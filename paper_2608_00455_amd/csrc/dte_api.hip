@@ -344,10 +344,12 @@ dte::ExtractParams extract_params(const float* p, const float* m, const float* v
     return a;
 }
 
-// Ordered-mode workspace: unordered entries, run records, wave totals and
-// bases, two counters; every part 256-byte aligned.
+// Ordered-mode workspace: per-wave regions (capacity entries in all), the
+// shared area for flushes that do not fit their region (capacity entries),
+// run records, wave totals, region fills and bases, two counters; every
+// part 256-byte aligned.
 struct OrderedWorkspace {
-    int64_t idx, val, runs, wave_count, wave_base, counters, total;
+    int64_t ridx, rval, idx, val, runs, wave_count, region_count, wave_base, counters, total;
     int64_t max_runs;
 };
 
@@ -358,11 +360,14 @@ OrderedWorkspace ordered_layout(int64_t capacity)
     OrderedWorkspace w;
     // every flush but a wave's last holds exactly 1024 entries
     w.max_runs = capacity / 1024 + dte::kMaxOrderedWaves + 1;
-    w.idx = 0;
+    w.ridx = 0;
+    w.rval = align256(w.ridx + capacity * (int64_t)sizeof(int64_t));
+    w.idx = align256(w.rval + capacity * (int64_t)sizeof(uint16_t));
     w.val = align256(w.idx + capacity * (int64_t)sizeof(int64_t));
     w.runs = align256(w.val + capacity * (int64_t)sizeof(uint16_t));
     w.wave_count = align256(w.runs + w.max_runs * (int64_t)sizeof(dte::OrderRun));
-    w.wave_base = align256(w.wave_count + dte::kMaxOrderedWaves * (int64_t)sizeof(int64_t));
+    w.region_count = align256(w.wave_count + dte::kMaxOrderedWaves * (int64_t)sizeof(int64_t));
+    w.wave_base = align256(w.region_count + dte::kMaxOrderedWaves * (int64_t)sizeof(int64_t));
     w.counters = align256(w.wave_base + dte::kMaxOrderedWaves * (int64_t)sizeof(int64_t));
     w.total = align256(w.counters + 2 * (int64_t)sizeof(int64_t));
     return w;
@@ -418,6 +423,10 @@ dte_status dte_extract_delta_ordered(const float* p, const float* m, const float
     a.max_runs = w.max_runs;
     a.run_cursor = counters + 1;
     a.wave_count = reinterpret_cast<int64_t*>(base + w.wave_count);
+    a.region_idx = reinterpret_cast<int64_t*>(base + w.ridx);
+    a.region_val = reinterpret_cast<uint16_t*>(base + w.rval);
+    a.region_count = reinterpret_cast<int64_t*>(base + w.region_count);
+    a.region_size = capacity / dte::extract_waves(a, cus);
     int32_t waves = 0;
     if (dte::launch_extract(a, cus, s, &waves) != hipSuccess) return DTE_ERR_HIP;
     dte::OrderParams o;
@@ -429,8 +438,11 @@ dte_status dte_extract_delta_ordered(const float* p, const float* m, const float
     o.waves = waves;
     o.src_idx = a.out_idx;
     o.src_val = a.out_val;
-    o.unordered_total = counters;
     o.src_capacity = capacity;
+    o.region_idx = a.region_idx;
+    o.region_val = a.region_val;
+    o.region_count = a.region_count;
+    o.region_size = a.region_size;
     o.out_idx = out_idx;
     o.out_val = out_val;
     o.capacity = capacity;

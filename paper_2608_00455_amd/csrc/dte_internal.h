@@ -74,12 +74,20 @@ struct ExtractParams {
     int64_t capacity;
     int64_t* cursor;
     float* out_prev;      // nullable
-    // ordered mode (runs != nullptr): every flush is recorded, every wave
-    // writes its entry total to wave_count[wave]
+    // ordered mode (runs != nullptr): wave g writes its first flushes to its
+    // own region [g region_size, (g+1) region_size) of region_idx/region_val
+    // (no atomics) and the number of entries there to region_count[g]; the
+    // flushes that no longer fit go to out_idx/out_val at positions from the
+    // cursor and are recorded in runs; every wave writes its entry total to
+    // wave_count[wave]
     OrderRun* runs;
     int64_t max_runs;
     int64_t* run_cursor;
     int64_t* wave_count;
+    int64_t* region_idx;
+    uint16_t* region_val;
+    int64_t* region_count;
+    int64_t region_size;      // entries per wave region
     int32_t wave0;        // global number of this launch's first wave
     // routing mode (route != 0): each flush sends its entries through the
     // plan into the receiver buckets (out, counts added to rank_count)
@@ -98,10 +106,14 @@ constexpr int kMaxOrderedWaves = 16384;
 hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream,
                           int32_t* waves = nullptr);
 
+// The number of waves launch_extract(a, cus, ...) launches.
+int64_t extract_waves(const ExtractParams& a, int cus);
+
 // Ordered mode, after launch_extract: wave_base[g] = *cursor + entries of
-// waves < g; copies every recorded run from the unordered arrays to
-// (out_idx, out_val) at wave_base[run.wave] + run.woff (positions below
-// capacity); then *cursor += *unordered_total.
+// waves < g; copies every wave's region part to (out_idx, out_val) at
+// wave_base[g] and every recorded run from the shared area at
+// wave_base[run.wave] + run.woff (positions below capacity); then *cursor
+// += the total of the wave counts.
 struct OrderParams {
     const OrderRun* runs;
     const int64_t* run_cursor;
@@ -111,8 +123,11 @@ struct OrderParams {
     int32_t waves;
     const int64_t* src_idx;
     const uint16_t* src_val;
-    const int64_t* unordered_total;
     int64_t src_capacity;
+    const int64_t* region_idx;
+    const uint16_t* region_val;
+    const int64_t* region_count;
+    int64_t region_size;
     int64_t* out_idx;
     uint16_t* out_val;
     int64_t capacity;

@@ -183,10 +183,14 @@ struct WaveStage {
     int32_t wave;     // global wave number
 };
 
-// Wave-uniform output state: entries staged in LDS, entries flushed so far.
+// Wave-uniform output state: entries staged in LDS, entries flushed so far;
+// ordered mode: entries written to the wave's region, and whether the region
+// is exhausted (then every later flush goes to the shared area).
 struct Staging {
     int staged;
     int64_t flushed;
+    int64_t in_region;
+    int spilled;
 };
 
 __device__ __forceinline__ void wave_sync()
@@ -241,6 +245,26 @@ __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging&
         so.staged = 0;
         wave_sync();
         return;
+    }
+    if (a.runs && !so.spilled) {
+        if (so.flushed + staged <= a.region_size) {
+            // ordered mode: the wave's own region, no atomics; a same-address
+            // atomic per flush slows the whole stream (its memory channel
+            // serves the reads of every wave)
+            const int64_t r0 = (int64_t)st.wave * a.region_size + so.flushed;
+            for (int i = lane; i < staged; i += 64) {
+                const uint32_t key = st.key[i];
+                const int64_t t = st.t_first + (int64_t)(key >> kTileBits);
+                a.region_idx[r0 + i] = a.index_base + t * kWaveTile + (key & (kWaveTile - 1));
+                a.region_val[r0 + i] = st.val[i];
+            }
+            so.flushed += staged;
+            so.in_region = so.flushed;
+            so.staged = 0;
+            wave_sync();
+            return;
+        }
+        so.spilled = 1;
     }
     unsigned long long base = 0;
     if (lane == 0) {
@@ -499,7 +523,7 @@ __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_
     const int64_t per = (last - first + nw - 1) / nw;
     const int64_t w_first = first + g * per;
     const int64_t w_last = (w_first + per < last) ? w_first + per : last;
-    Staging so{0, 0};
+    Staging so{0, 0, 0, 0};
     const WaveStage st{s_key[wave], s_val[wave], s_qp[wave], s_qm[wave], s_qv[wave],
                        s_qkey[wave], w_first, a.wave0 + (int32_t)g};
     uint32_t iter = 0;
@@ -512,7 +536,10 @@ __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_
     }
     if (queued > 0) drain_queue<kDecayOne, kLit, kRoute>(a, st, queued, so, lane);
     if (so.staged > 0) flush_wave<kRoute>(a, st, so, lane);
-    if (a.runs && lane == 0) a.wave_count[st.wave] = so.flushed;
+    if (a.runs && lane == 0) {
+        a.wave_count[st.wave] = so.flushed;
+        a.region_count[st.wave] = so.in_region;
+    }
 }
 
 template <bool kVecLoads>
@@ -596,7 +623,7 @@ int32_t launch_all(const ExtractParams& a, bool vec, int64_t max_grid, hipStream
 // ---- ordered mode: runs to ascending positions ----------------------------
 
 // One block: wave_base = *cursor + exclusive prefix of the wave totals; then
-// the cursor advances by the true total of the call.
+// the cursor advances by their sum, the true total of the call.
 __global__ __launch_bounds__(1024) void order_scan_kernel(OrderParams o)
 {
     constexpr int kThreads = 1024;
@@ -624,16 +651,50 @@ __global__ __launch_bounds__(1024) void order_scan_kernel(OrderParams o)
         }
     }
     __syncthreads();                              // every thread has read the cursor
-    if (tid == 0) *o.cursor = c0 + *o.unordered_total;
+    if (tid == 0) *o.cursor = c0 + part[kThreads - 1];
 }
 
-// Each wave copies whole runs: entry i of a run moves from src + i to
-// wave_base[wave] + woff + i.
+constexpr int kCopySlots = 8;                  // entries per lane per copy chunk
+constexpr int kCopyChunk = 64 * kCopySlots;
+
+// Regions: the waves take chunks of kCopyChunk entries (chunk c of extract
+// wave g's region: its entries c kCopyChunk + i, which move to wave_base[g]
+// + c kCopyChunk + i), all loads of a chunk before its stores.  Then whole
+// recorded runs: entry i of a run moves from src + i to wave_base[wave] +
+// woff + i.
 __global__ __launch_bounds__(kBlock) void order_copy_kernel(OrderParams o)
 {
     const int lane = threadIdx.x & 63;
     const int64_t w = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
     const int64_t nw = (int64_t)gridDim.x * kWaves;
+    const int64_t per_region = (o.region_size + kCopyChunk - 1) / kCopyChunk;
+    const int64_t chunks = (int64_t)o.waves * per_region;
+    const int64_t* __restrict__ ridx = o.region_idx;
+    const uint16_t* __restrict__ rval = o.region_val;
+    for (int64_t k = w; k < chunks; k += nw) {
+        const int64_t g = k / per_region;
+        const int64_t c0 = (k - g * per_region) * kCopyChunk;
+        const int64_t cnt = o.region_count[g];
+        if (c0 >= cnt) continue;
+        const int64_t src0 = g * o.region_size + c0;
+        const int64_t dst0 = o.wave_base[g] + c0;
+        int64_t x[kCopySlots];
+        uint16_t y[kCopySlots];
+#pragma unroll
+        for (int j = 0; j < kCopySlots; ++j) {
+            const int64_t i = j * 64 + lane;
+            x[j] = c0 + i < cnt ? ridx[src0 + i] : 0;
+            y[j] = c0 + i < cnt ? rval[src0 + i] : (uint16_t)0;
+        }
+#pragma unroll
+        for (int j = 0; j < kCopySlots; ++j) {
+            const int64_t i = j * 64 + lane;
+            if (c0 + i < cnt && dst0 + i < o.capacity) {
+                o.out_idx[dst0 + i] = x[j];
+                o.out_val[dst0 + i] = y[j];
+            }
+        }
+    }
     int64_t nruns = *o.run_cursor;
     if (nruns > o.max_runs) nruns = o.max_runs;
     for (int64_t r = w; r < nruns; r += nw) {
@@ -656,19 +717,52 @@ hipError_t launch_order(const OrderParams& o, int cus, hipStream_t stream)
 {
     if (o.waves <= 0) return hipSuccess;
     hipLaunchKernelGGL(order_scan_kernel, dim3(1), dim3(1024), 0, stream, o);
-    hipLaunchKernelGGL(order_copy_kernel, dim3((unsigned)cus * 4), dim3(kBlock), 0, stream, o);
+    hipLaunchKernelGGL(order_copy_kernel, dim3((unsigned)cus * 8), dim3(kBlock), 0, stream, o);
     return hipGetLastError();
+}
+
+namespace {
+
+// Waves that launch_all launches (its grid rule).
+int64_t waves_of(int64_t n, bool vec, int64_t max_grid)
+{
+    const auto blocks = [max_grid](int64_t first, int64_t last) -> int64_t {
+        if (last <= first) return 0;
+        const int64_t b = (last - first + kWaves - 1) / kWaves;
+        return b < max_grid ? b : max_grid;
+    };
+    const int64_t full = n / kWaveTile;
+    const int64_t ntiles = (n + kWaveTile - 1) / kWaveTile;
+    return (vec ? blocks(0, full) + blocks(full, ntiles) : blocks(0, ntiles)) * kWaves;
+}
+
+int64_t max_grid_of(const ExtractParams& a, int cus)
+{
+    int64_t max_grid = (int64_t)cus * kBlocksPerCU;
+    // ordered mode: both launches together stay within kMaxOrderedWaves
+    if (a.runs && max_grid > kMaxOrderedWaves / kWaves - 1) max_grid = kMaxOrderedWaves / kWaves - 1;
+    return max_grid;
+}
+
+bool vector_loads(const ExtractParams& a)
+{
+    return aligned16(a.p) && aligned16(a.m) && aligned16(a.v) &&
+           (a.out_prev == nullptr || aligned16(a.out_prev));
+}
+
+}  // namespace
+
+int64_t extract_waves(const ExtractParams& a, int cus)
+{
+    return a.n > 0 ? waves_of(a.n, vector_loads(a), max_grid_of(a, cus)) : 0;
 }
 
 hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream, int32_t* waves)
 {
     if (waves) *waves = 0;
     if (a.n <= 0) return hipSuccess;
-    int64_t max_grid = (int64_t)cus * kBlocksPerCU;
-    // ordered mode: both launches together stay within kMaxOrderedWaves
-    if (a.runs && max_grid > kMaxOrderedWaves / kWaves - 1) max_grid = kMaxOrderedWaves / kWaves - 1;
-    const bool vec = aligned16(a.p) && aligned16(a.m) && aligned16(a.v) &&
-                     (a.out_prev == nullptr || aligned16(a.out_prev));
+    const int64_t max_grid = max_grid_of(a, cus);
+    const bool vec = vector_loads(a);
     int32_t w;
     const bool one = a.decay == 1.0f;
     if (a.route) {

@@ -2,11 +2,10 @@
 """Throughput of the delta-extraction hot path on one MI355X.
 
 One step = one pass of the whole path over the trainer shard already
-resident in HBM: reset the delta cursor, dte_extract_delta_ordered (AdamW
-inversion + BF16 change detection + compaction into an ascending delta;
---unordered: dte_extract_delta, whose runs land in any order), dte_remap
-(receiver coordinates) and dte_apply (scatter into the receiver BF16
-shards).
+resident in HBM: reset the delta cursor, dte_extract_delta (AdamW
+inversion + BF16 change detection + compaction; --ordered:
+dte_extract_delta_ordered, an ascending delta), dte_remap (receiver
+coordinates) and dte_apply (scatter into the receiver BF16 shards).
 
 Default workload: the full Qwen3-8B state (8,190,735,360 fp32 elements of
 theta, m, v; receiver TP=4).  Prints one JSON line with the throughput in
@@ -192,9 +191,8 @@ def main():
     ap.add_argument("--fused", action="store_true",
                     help="dte_extract_remap (detection routed straight into the buckets) "
                          "instead of dte_extract_delta + dte_remap")
-    ap.add_argument("--unordered", action="store_true",
-                    help="dte_extract_delta (runs of the delta in any order) instead of "
-                         "dte_extract_delta_ordered (ascending, deterministic delta)")
+    ap.add_argument("--ordered", action="store_true",
+                    help="dte_extract_delta_ordered (ascending, deterministic delta)")
     ap.add_argument("--norm-group", action="store_true",
                     help="norms in a parameter group without weight decay")
     ap.add_argument("--capacity-fraction", type=float, default=None,
@@ -248,7 +246,7 @@ def main():
     if frac is None:
         frac = 0.25 if args.workload == "qwen3_8b_4l_tp4" else 0.02
     cap = max(1 << 20, int(n * frac))
-    ordered = not (args.unordered or args.fused)
+    ordered = bool(args.ordered)
     pipe = DeltaPipeline(spec, capacity=cap, ordered=ordered)
     runs = group_runs(wl, hp)
     stream = torch.cuda.current_stream()
@@ -343,8 +341,8 @@ def main():
         step_bytes = 12 * n + 10 * changed + 10 * changed + 10 * routed + 12 * routed
     achieved = k_bytes / (k_ms / 1e3) / 1e9
     # the counters were taken for the default configuration only (folded
-    # order, ordered output, one parameter group)
-    default_mode = not (args.unordered or args.fused or args.literal or args.norm_group)
+    # order, unordered output, one parameter group)
+    default_mode = not (args.ordered or args.fused or args.literal or args.norm_group)
     out = {
         "metric": "delta-extract+remap+apply: elements/s and HBM GB/s (% of peak), "
                   "Qwen3-8B shape",
@@ -368,7 +366,7 @@ def main():
                    "step_frac_of_hbm_peak": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS},
         "roofline": {"kernel": kernel, "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": (measured_traffic(wl.name, kernel, "ordered")
+                     "traffic": (measured_traffic(wl.name, kernel, "unordered")
                                  if default_mode else None),
                      "kernel_ms": k_ms,
                      "bytes_per_launch": k_bytes},

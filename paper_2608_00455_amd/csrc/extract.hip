@@ -248,9 +248,8 @@ __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging&
     }
     if (a.runs && !so.spilled) {
         if (so.flushed + staged <= a.region_size) {
-            // ordered mode: the wave's own region, no atomics; a same-address
-            // atomic per flush slows the whole stream (its memory channel
-            // serves the reads of every wave)
+            // ordered mode: the wave's own region, no atomics (reservations
+            // that every wave takes from one address slow the whole stream)
             const int64_t r0 = (int64_t)st.wave * a.region_size + so.flushed;
             for (int i = lane; i < staged; i += 64) {
                 const uint32_t key = st.key[i];

@@ -515,3 +515,50 @@ def test_fused_extract_remap_rejects_plans_over_16_ranks():
         pipe.extract_remap(p, p, p, wl.hp)
     assert e.value.status == B.DTE_ERR_ARG
     pipe.close()
+
+
+@pytest.mark.parametrize("slack", [0, 1000])
+def test_ordered_extract_when_waves_outgrow_their_regions(slack):
+    """All changes in the first half of the range (no moments in the second
+    half): with a tight capacity each wave's region holds about the mean
+    number of entries per wave, so the waves of the first half write their
+    first runs to their regions and the later ones through the shared area;
+    the delta must still equal the oracle's, in ascending order.  (50 M
+    elements: about 2,300 entries per wave there, regions of about 1,150.)"""
+    n = 3 << 24
+    hp = W.StepHP(lr=1e-4, weight_decay=0.0)
+    sc = ocore.derive_scalars(hp)
+    rng = np.random.default_rng(26080455 + 44)
+    z = lambda: rng.standard_normal(n, dtype=np.float32)  # noqa: E731
+    p_prev = np.float32(0.02) * z()
+    m_prev = np.float32(1e-4) * z()
+    v_prev = np.abs(np.float32(1e-6) * z())
+    g = np.float32(1e-3) * z()
+    m_prev[n // 2:] = 0
+    g[n // 2:] = 0
+    p, m, v = ocore.adamw_forward(p_prev, m_prev, v_prev, g, sc)
+    idx, val, _ = ocore.detect(p, m, v, sc)
+    say("case: ordered extract, skewed delta", idx.size, slack)
+    # (the second half keeps a few changes: draws of -0.0, whose inverse
+    # with a zero step is +0.0, a different BF16 pattern)
+    assert idx.size > 0 and np.count_nonzero(idx >= n // 2) < 100
+    cap = idx.size + slack
+    tidx = torch.empty(cap, dtype=torch.int64, device="cuda")
+    tval = torch.empty(cap, dtype=torch.int16, device="cuda")
+    cur = torch.zeros(1, dtype=torch.int64, device="cuda")
+    ws = torch.empty(B.dte_ordered_workspace_bytes(cap), dtype=torch.uint8, device="cuda")
+    tp, tm, tv = dev(p), dev(m), dev(v)
+    for _ in range(2):
+        cur.zero_()
+        B.dte_extract_delta_ordered(tp.data_ptr(), tm.data_ptr(), tv.data_ptr(), n, 0, hp,
+                                    tidx.data_ptr(), tval.data_ptr(), cap, cur.data_ptr(),
+                                    ws.data_ptr(), ws.numel())
+        sync()
+        assert int(cur.item()) == idx.size
+        got_i = tidx[:idx.size].cpu().numpy()
+        got_v = tval[:idx.size].cpu().numpy().view(np.uint16)
+        assert np.array_equal(got_i, idx) and np.array_equal(got_v, val)
+        # white box: the workspace's last 256 bytes hold the shared area's
+        # counters (entries, runs); both paths were taken
+        shared_entries, shared_runs = ws[-256:-240].cpu().numpy().view(np.int64).tolist()
+        assert shared_runs > 0 and 0 < shared_entries < idx.size

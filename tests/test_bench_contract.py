@@ -1,0 +1,45 @@
+"""Host-side checks of bench.py: the one-GPU rule and the traffic record
+lookup (no GPU needed)."""
+import hashlib
+import json
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_traffic_record_lookup():
+    path = os.path.join(ROOT, "profiles", "extract_qwen3_8b_tp4_traffic.json")
+    rec = json.load(open(path))
+    src = os.path.join(ROOT, rec["kernel_source"])
+    got = bench.measured_traffic("qwen3_8b_tp4", "extract", rec["mode"])
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["kernel_source_sha256"]:
+        # the kernel changed since the counters were taken: bench reports null
+        assert got is None
+        return
+    assert got == rec["traffic_bytes_per_launch"]
+    # the fetch and write counters, scaled by the copy calibration, give the total
+    cal = rec["copy_calibration"]
+    total = (sum(rec["fetch_size_kib_per_call"].values()) * 1024 * cal["fetch_factor"] +
+             sum(rec["write_size_kib_per_call"].values()) * 1024 * cal["write_factor"])
+    assert abs(total - got) < 1.0
+    # within a fraction of a percent of extract's algorithmic bytes 12 N + 10 M
+    algorithmic = 12 * 8190735360 + 10 * 25978374
+    assert 1.0 <= got / algorithmic < 1.01
+
+
+def test_traffic_is_withheld_for_another_mode_or_workload():
+    assert bench.measured_traffic("qwen3_8b_tp4", "extract", "no such mode") is None
+    assert bench.measured_traffic("tiny_block_tp2", "extract", "unordered") is None

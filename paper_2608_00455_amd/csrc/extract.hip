@@ -169,6 +169,7 @@ __device__ __forceinline__ float exact_prev(float p, float m, float v, const Ext
 }
 
 constexpr int kTileBits = __builtin_ctz(kWaveTile);
+constexpr int64_t kDenseRatio = 64;             // see flush_wave
 static_assert((1 << kTileBits) == kWaveTile, "wave tile must be a power of two");
 // Per-wave LDS areas.  Keys are (wave iteration << kTileBits) | element in
 // the tile; the wave's tiles are t_first + iteration.
@@ -198,6 +199,28 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Write staged entries [0, staged) to out_idx / out_val from position
+// base, dropping those at or beyond capacity; kStream: offsets with
+// non-temporal stores.
+template <bool kStream>
+__device__ __forceinline__ void write_out(const ExtractParams& a, const WaveStage& st, int64_t base,
+                                          int staged, int lane)
+{
+    for (int i = lane; i < staged; i += 64) {
+        const int64_t pos = base + i;
+        if (pos < a.capacity) {
+            const uint32_t key = st.key[i];
+            const int64_t t = st.t_first + (int64_t)(key >> kTileBits);
+            const int64_t x = a.index_base + t * kWaveTile + (int64_t)(key & (kWaveTile - 1));
+            if (kStream)
+                __builtin_nontemporal_store(x, a.out_idx + pos);
+            else
+                a.out_idx[pos] = x;
+            a.out_val[pos] = st.val[i];
+        }
+    }
 }
 
 // Copy a wave's staged LDS entries to the reserved global range (and, in
@@ -283,15 +306,16 @@ __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging&
         }
     }
     base = __shfl(base, 0);
-    for (int i = lane; i < staged; i += 64) {
-        const int64_t pos = (int64_t)base + i;
-        if (pos < a.capacity) {
-            const uint32_t key = st.key[i];
-            const int64_t t = st.t_first + (int64_t)(key >> kTileBits);
-            a.out_idx[pos] = a.index_base + t * kWaveTile + (key & (kWaveTile - 1));
-            a.out_val[pos] = st.val[i];
-        }
-    }
+    // a wave that has so far found more than one changed element per
+    // kDenseRatio elements scanned writes its offsets with non-temporal
+    // stores (measured faster on deltas of several percent of the state,
+    // slower on sparse ones); the choice is wave-uniform
+    const uint32_t last = __builtin_amdgcn_readfirstlane(st.key[staged - 1]);
+    const int64_t scanned = ((int64_t)(last >> kTileBits) + 1) * kWaveTile;
+    if ((so.flushed + staged) * kDenseRatio > scanned)
+        write_out<true>(a, st, (int64_t)base, staged, lane);
+    else
+        write_out<false>(a, st, (int64_t)base, staged, lane);
     so.flushed += staged;
     so.staged = 0;
     wave_sync();   // the staging area is rewritten next: finish these reads first

@@ -18,7 +18,9 @@
  *    synchronisation, no host<->device copies.
  *  - Return value: DTE_OK, or an error code; dte_status_string() names it.
  *    Argument errors are detected on the host before anything is enqueued.
- *    The library never aborts and never throws across this interface.
+ *    The library never aborts and never throws across this interface: a
+ *    call that builds host tables or starts host threads returns
+ *    DTE_ERR_HOST when host memory or a thread cannot be obtained.
  *  - Sizes are element counts (int64).  Zero-length inputs are legal and
  *    enqueue nothing.
  *  - Floating point: IEEE binary32, round-to-nearest-even, no fused
@@ -44,6 +46,7 @@ typedef int32_t dte_status;
 #define DTE_ERR_CORRUPT 6  /* stored data failed its checksum or format check */
 #define DTE_ERR_CHAIN 7    /* a stored version does not extend the local base version */
 #define DTE_ERR_UNSUPPORTED 8 /* the requested codec is not available on this host */
+#define DTE_ERR_HOST 9     /* a host resource (memory, a thread) could not be obtained */
 
 #define DTE_MAX_DIMS 4     /* tensor rank limit of segments and plan operations */
 #define DTE_MAX_RANKS 64   /* receiver ranks per plan */
@@ -210,9 +213,12 @@ typedef struct dte_plan dte_plan;
  *    element per rank), and together the segment's boxes cover every
  *    element (no change can be lost).
  * A canonical element may go to several ranks (replication).
- * *out receives the plan; the caller releases it with dte_plan_destroy.
- * Errors: DTE_ERR_ARG, DTE_ERR_PLAN, DTE_ERR_HIP.  Allocates device memory;
- * not a hot-path call. */
+ * *out receives the plan (NULL on error); the caller releases it with
+ * dte_plan_destroy.  The plan belongs to the device current at creation:
+ * dte_remap, dte_extract_remap and dte_apply return DTE_ERR_ARG when called
+ * with another current device.
+ * Errors: DTE_ERR_ARG, DTE_ERR_PLAN, DTE_ERR_HIP, DTE_ERR_HOST.  Allocates
+ * device memory; not a hot-path call. */
 dte_status dte_plan_create(const dte_segment* segs, int32_t nseg, const dte_op* ops,
                            int32_t nop, int32_t nranks, const int64_t* rank_numel,
                            dte_plan** out);

@@ -33,7 +33,8 @@
  *
  * Conventions of dte.h apply; these calls allocate, synchronise and do file
  * I/O (they are not hot-path calls).  Errors: DTE_ERR_ARG, DTE_ERR_IO,
- * DTE_ERR_CORRUPT, DTE_ERR_CHAIN, DTE_ERR_UNSUPPORTED, DTE_ERR_HIP.
+ * DTE_ERR_CORRUPT, DTE_ERR_CHAIN, DTE_ERR_UNSUPPORTED, DTE_ERR_HIP,
+ * DTE_ERR_HOST.
  */
 #ifndef DTE_STORE_H
 #define DTE_STORE_H

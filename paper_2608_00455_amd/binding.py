@@ -12,7 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdte.so")
 
 DTE_OK, DTE_ERR_ARG, DTE_ERR_PLAN, DTE_ERR_CAPACITY, DTE_ERR_HIP = 0, 1, 2, 3, 4
-DTE_ERR_IO, DTE_ERR_CORRUPT, DTE_ERR_CHAIN, DTE_ERR_UNSUPPORTED = 5, 6, 7, 8
+DTE_ERR_IO, DTE_ERR_CORRUPT, DTE_ERR_CHAIN, DTE_ERR_UNSUPPORTED, DTE_ERR_HOST = 5, 6, 7, 8, 9
 DTE_MAX_DIMS = 4
 DTE_MAX_RANKS = 64
 

@@ -7,9 +7,10 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
-#include <new>
+#include <memory>
 #include <vector>
 
+#include "abi_guard.h"
 #include "dte_internal.h"
 
 struct dte_plan {
@@ -38,6 +39,14 @@ int cu_count(int device)
         cache[device] = n;
     }
     return cache[device];
+}
+
+// The plan's tables live on the device it was created on; the hot calls
+// launch on the current device, which must be that one.
+bool on_plan_device(const dte_plan* plan)
+{
+    int dev = -1;
+    return hipGetDevice(&dev) == hipSuccess && dev == plan->device;
 }
 
 int current_cus()
@@ -276,6 +285,7 @@ const char* dte_status_string(dte_status status)
     case DTE_ERR_CORRUPT: return "DTE_ERR_CORRUPT: stored data failed its checksum or format check";
     case DTE_ERR_CHAIN: return "DTE_ERR_CHAIN: version does not extend the local base version";
     case DTE_ERR_UNSUPPORTED: return "DTE_ERR_UNSUPPORTED: codec not available";
+    case DTE_ERR_HOST: return "DTE_ERR_HOST: host memory or thread could not be obtained";
     default: return "unknown dte_status";
     }
 }
@@ -480,12 +490,16 @@ dte_status dte_adamw_forward(float* p, float* m, float* v, const float* g, int64
                : DTE_ERR_HIP;
 }
 
-dte_status dte_plan_create(const dte_segment* segs, int32_t nseg, const dte_op* ops,
-                           int32_t nop, int32_t nranks, const int64_t* rank_numel,
-                           dte_plan** out)
+}  // extern "C"
+
+namespace {
+
+// dte_plan_create after its null-pointer check; host containers may throw
+// (the caller turns that into DTE_ERR_HOST), and nothing is allocated on the
+// device until every host table is built.
+dte_status plan_create(const dte_segment* segs, int32_t nseg, const dte_op* ops, int32_t nop,
+                       int32_t nranks, const int64_t* rank_numel, dte_plan** out)
 {
-    if (!out) return DTE_ERR_ARG;
-    *out = nullptr;
     if (!segs || nseg < 1 || nop < 0 || (nop > 0 && !ops) || nranks < 1 ||
         nranks > DTE_MAX_RANKS || !rank_numel)
         return DTE_ERR_ARG;
@@ -551,13 +565,6 @@ dte_status dte_plan_create(const dte_segment* segs, int32_t nseg, const dte_op* 
     const size_t o_look = align_up(o_ops + dops.size() * sizeof(dte::DevOp));
     const size_t bytes = align_up(o_look + lookup.size() * sizeof(int32_t));
 
-    dte_plan* plan = new (std::nothrow) dte_plan;
-    if (!plan) return DTE_ERR_ARG;
-    plan->dev_mem = nullptr;
-    if (hipGetDevice(&plan->device) != hipSuccess || hipMalloc(&plan->dev_mem, bytes) != hipSuccess) {
-        delete plan;
-        return DTE_ERR_HIP;
-    }
     std::vector<unsigned char> img(bytes, 0);
     std::memcpy(img.data() + o_begin, seg_begin.data(), seg_begin.size() * sizeof(int64_t));
     std::memcpy(img.data() + o_shape, seg_shape.data(), seg_shape.size() * sizeof(uint32_t));
@@ -565,9 +572,13 @@ dte_status dte_plan_create(const dte_segment* segs, int32_t nseg, const dte_op* 
     std::memcpy(img.data() + o_sops, seg_ops.data(), seg_ops.size() * sizeof(int32_t));
     std::memcpy(img.data() + o_ops, dops.data(), dops.size() * sizeof(dte::DevOp));
     std::memcpy(img.data() + o_look, lookup.data(), lookup.size() * sizeof(int32_t));
+    std::unique_ptr<dte_plan> plan(new dte_plan);
+    plan->dev_mem = nullptr;
+    plan->rank_numel.assign(rank_numel, rank_numel + nranks);
+    if (hipGetDevice(&plan->device) != hipSuccess || hipMalloc(&plan->dev_mem, bytes) != hipSuccess)
+        return DTE_ERR_HIP;
     if (hipMemcpy(plan->dev_mem, img.data(), bytes, hipMemcpyHostToDevice) != hipSuccess) {
         (void)hipFree(plan->dev_mem);
-        delete plan;
         return DTE_ERR_HIP;
     }
     unsigned char* base = static_cast<unsigned char*>(plan->dev_mem);
@@ -586,9 +597,22 @@ dte_status dte_plan_create(const dte_segment* segs, int32_t nseg, const dte_op* 
     plan->nranks = nranks;
     plan->max_replication = max_rep;
     plan->total = total;
-    plan->rank_numel.assign(rank_numel, rank_numel + nranks);
-    *out = plan;
+    *out = plan.release();
     return DTE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dte_status dte_plan_create(const dte_segment* segs, int32_t nseg, const dte_op* ops,
+                           int32_t nop, int32_t nranks, const int64_t* rank_numel,
+                           dte_plan** out)
+{
+    if (!out) return DTE_ERR_ARG;
+    *out = nullptr;
+    return dte::no_throw(
+        [&] { return plan_create(segs, nseg, ops, nop, nranks, rank_numel, out); });
 }
 
 void dte_plan_destroy(dte_plan* plan)
@@ -614,7 +638,7 @@ dte_status dte_remap(const dte_plan* plan, const int64_t* idx, const uint16_t* v
                      int64_t* rank_count, void* stream)
 {
     if (!plan || !count || !out_off || !out_val || !rank_capacity || !rank_count ||
-        in_capacity < 0)
+        in_capacity < 0 || !on_plan_device(plan))
         return DTE_ERR_ARG;
     if (in_capacity > 0 && (!idx || !val)) return DTE_ERR_ARG;
     for (int32_t r = 0; r < plan->nranks; ++r) {
@@ -648,7 +672,7 @@ dte_status dte_extract_remap(const float* p, const float* m, const float* v, int
                              void* stream)
 {
     if (!plan || !out_off || !out_val || !rank_capacity || !rank_count ||
-        plan->nranks > dte::kRanksPerLaunch)
+        plan->nranks > dte::kRanksPerLaunch || !on_plan_device(plan))
         return DTE_ERR_ARG;
     if (!extract_args_ok(p, m, v, n, index_base, hp, nullptr, nullptr, 0, count))
         return DTE_ERR_ARG;
@@ -679,7 +703,8 @@ dte_status dte_apply(const dte_plan* plan, uint16_t* const* shards, const int64_
                      const uint16_t* const* val, const int64_t* rank_count,
                      const int64_t* rank_capacity, void* stream)
 {
-    if (!plan || !shards || !off || !val || !rank_count || !rank_capacity) return DTE_ERR_ARG;
+    if (!plan || !shards || !off || !val || !rank_count || !rank_capacity || !on_plan_device(plan))
+        return DTE_ERR_ARG;
     for (int32_t r = 0; r < plan->nranks; ++r) {
         if (rank_capacity[r] < 0) return DTE_ERR_ARG;
         if (rank_capacity[r] > 0 && (!off[r] || !val[r])) return DTE_ERR_ARG;

@@ -34,6 +34,7 @@
 #include <vector>
 
 #include "../../include/dte_store.h"
+#include "abi_guard.h"
 
 namespace {
 
@@ -516,23 +517,39 @@ bool options_ok(const dte_store_options* o)
            o->chunk_entries >= 1 && o->chunk_entries <= ((int64_t)1 << 26);
 }
 
+// First status other than DTE_OK reported by any thread.
+struct FirstError {
+    std::mutex m;
+    dte_status st = DTE_OK;
+    void set(dte_status s)
+    {
+        std::lock_guard<std::mutex> g(m);
+        if (st == DTE_OK) st = s;
+    }
+    dte_status get()
+    {
+        std::lock_guard<std::mutex> g(m);
+        return st;
+    }
+};
+
 // ---- a fixed pool of host threads -------------------------------------------
 
+// A job that throws reports DTE_ERR_HOST to `err`; if a thread cannot be
+// started, the threads already running are joined before the constructor
+// rethrows.
 class Pool {
 public:
-    explicit Pool(int n)
+    Pool(int n, FirstError& err) : err_(err)
     {
-        for (int i = 0; i < n; ++i) th_.emplace_back([this] { loop(); });
-    }
-    ~Pool()
-    {
-        {
-            std::lock_guard<std::mutex> g(m_);
-            stop_ = true;
+        try {
+            for (int i = 0; i < n; ++i) th_.emplace_back([this] { loop(); });
+        } catch (...) {
+            finish();
+            throw;
         }
-        cv_.notify_all();
-        for (auto& t : th_) t.join();
     }
+    ~Pool() { finish(); }
     void push(std::function<void()> f)
     {
         {
@@ -554,9 +571,24 @@ private:
                 f = std::move(q_.front());
                 q_.pop_front();
             }
-            f();
+            try {
+                f();
+            } catch (...) {
+                err_.set(DTE_ERR_HOST);
+            }
         }
     }
+    void finish()
+    {
+        {
+            std::lock_guard<std::mutex> g(m_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        for (auto& t : th_) t.join();
+        th_.clear();
+    }
+    FirstError& err_;
     std::vector<std::thread> th_;
     std::deque<std::function<void()>> q_;
     std::mutex m_;
@@ -610,22 +642,6 @@ private:
     std::mutex m_;
     std::condition_variable cv_;
     bool ok_ = true;
-};
-
-// First status other than DTE_OK reported by any thread.
-struct FirstError {
-    std::mutex m;
-    dte_status st = DTE_OK;
-    void set(dte_status s)
-    {
-        std::lock_guard<std::mutex> g(m);
-        if (st == DTE_OK) st = s;
-    }
-    dte_status get()
-    {
-        std::lock_guard<std::mutex> g(m);
-        return st;
-    }
 };
 
 // ---- device kernels ---------------------------------------------------------
@@ -928,7 +944,7 @@ dte_status read_chunks(const std::string& dir, const Manifest& m, int32_t thread
 {
     FirstError err;
     {
-        Pool pool(threads);
+        Pool pool(threads, err);
         for (size_t k = 0; k < m.chunks.size(); ++k) {
             pool.push([&, k] {
                 if (err.get() != DTE_OK) return;
@@ -1009,7 +1025,7 @@ dte_status write_host_impl(const char* dir, int64_t version, int32_t writer,
     int64_t published = 0;
     for (const ChunkJob& j : jobs) published += j.count;
     {
-        Pool pool(opt->threads);
+        Pool pool(opt->threads, err);
         for (size_t k = 0; k < jobs.size(); ++k) {
             pool.push([&, k] {
                 const ChunkJob& j = jobs[k];
@@ -1107,7 +1123,7 @@ dte_status write_device_impl(const char* dir, int64_t version, int32_t writer,
     std::mutex mm;
     FirstError err;
     {
-        Pool pool(opt->threads);
+        Pool pool(opt->threads, err);
         for (size_t k = 0; k < jobs.size() && err.get() == DTE_OK; ++k) {
             const ChunkJob j = jobs[k];
             const int slot = ring.acquire();
@@ -1141,9 +1157,11 @@ dte_status dte_store_write_part_host(const char* dir, int64_t version, int32_t w
                                      const int64_t* idx, const uint16_t* val, int64_t count,
                                      const dte_store_options* opt, dte_store_stats* stats)
 {
-    if (!common_write_args(dir, version, writer, segs, nseg, opt)) return DTE_ERR_ARG;
-    const std::vector<Segment> sg = to_segments(segs, nseg);
-    return write_host_impl(dir, version, writer, sg, identity_pieces(sg), idx, val, count, opt, stats);
+    return dte::no_throw([&]() -> dte_status {
+        if (!common_write_args(dir, version, writer, segs, nseg, opt)) return DTE_ERR_ARG;
+        const std::vector<Segment> sg = to_segments(segs, nseg);
+        return write_host_impl(dir, version, writer, sg, identity_pieces(sg), idx, val, count, opt, stats);
+    });
 }
 
 dte_status dte_store_write_part_host_mapped(const char* dir, int64_t version, int32_t writer,
@@ -1152,11 +1170,13 @@ dte_status dte_store_write_part_host_mapped(const char* dir, int64_t version, in
                                             const int64_t* idx, const uint16_t* val, int64_t count,
                                             const dte_store_options* opt, dte_store_stats* stats)
 {
-    if (!common_write_args(dir, version, writer, segs, nseg, opt) || npiece < 0 ||
-        (npiece > 0 && !pieces))
-        return DTE_ERR_ARG;
-    return write_host_impl(dir, version, writer, to_segments(segs, nseg), to_pieces(pieces, npiece),
-                           idx, val, count, opt, stats);
+    return dte::no_throw([&]() -> dte_status {
+        if (!common_write_args(dir, version, writer, segs, nseg, opt) || npiece < 0 ||
+            (npiece > 0 && !pieces))
+            return DTE_ERR_ARG;
+        return write_host_impl(dir, version, writer, to_segments(segs, nseg), to_pieces(pieces, npiece),
+                               idx, val, count, opt, stats);
+    });
 }
 
 dte_status dte_store_write_part_device(const char* dir, int64_t version, int32_t writer,
@@ -1166,10 +1186,12 @@ dte_status dte_store_write_part_device(const char* dir, int64_t version, int32_t
                                        const dte_store_options* opt, dte_store_stats* stats,
                                        void* stream)
 {
-    if (!common_write_args(dir, version, writer, segs, nseg, opt)) return DTE_ERR_ARG;
-    const std::vector<Segment> sg = to_segments(segs, nseg);
-    return write_device_impl(dir, version, writer, sg, identity_pieces(sg), idx, val, count, capacity,
-                             opt, stats, stream);
+    return dte::no_throw([&]() -> dte_status {
+        if (!common_write_args(dir, version, writer, segs, nseg, opt)) return DTE_ERR_ARG;
+        const std::vector<Segment> sg = to_segments(segs, nseg);
+        return write_device_impl(dir, version, writer, sg, identity_pieces(sg), idx, val, count, capacity,
+                                 opt, stats, stream);
+    });
 }
 
 dte_status dte_store_write_part_device_mapped(const char* dir, int64_t version, int32_t writer,
@@ -1180,118 +1202,126 @@ dte_status dte_store_write_part_device_mapped(const char* dir, int64_t version, 
                                               const dte_store_options* opt, dte_store_stats* stats,
                                               void* stream)
 {
-    if (!common_write_args(dir, version, writer, segs, nseg, opt) || npiece < 0 ||
-        (npiece > 0 && !pieces))
-        return DTE_ERR_ARG;
-    return write_device_impl(dir, version, writer, to_segments(segs, nseg), to_pieces(pieces, npiece),
-                             idx, val, count, capacity, opt, stats, stream);
+    return dte::no_throw([&]() -> dte_status {
+        if (!common_write_args(dir, version, writer, segs, nseg, opt) || npiece < 0 ||
+            (npiece > 0 && !pieces))
+            return DTE_ERR_ARG;
+        return write_device_impl(dir, version, writer, to_segments(segs, nseg), to_pieces(pieces, npiece),
+                                 idx, val, count, capacity, opt, stats, stream);
+    });
 }
 
 dte_status dte_store_commit(const char* dir, int64_t version, int64_t parent, int32_t nwriters,
                             int32_t* committed)
 {
-    if (!dir || version < 1 || parent < 0 || parent >= version || nwriters < 1 || nwriters > 4096 ||
-        !committed)
-        return DTE_ERR_ARG;
-    *committed = 0;
-    const std::string d(dir), vd = vdir(d, version);
-    std::vector<Segment> segs;
-    std::vector<ChunkMeta> chunks;
-    std::string codec;
-    int64_t entries = 0;
-    for (int32_t w = 0; w < nwriters; ++w) {
-        std::vector<uint8_t> text;
-        if (!read_file(vd + "/part-" + std::to_string(w) + ".json", text)) return DTE_ERR_IO;
-        Json j;
-        int64_t v = 0, wr = 0, e = 0;
-        std::vector<Segment> ps;
-        std::vector<ChunkMeta> pc;
-        const Json* c = nullptr;
-        if (!parse_json(text, j) || !int_of(j, "version", v) || !int_of(j, "writer", wr) ||
-            !int_of(j, "entries", e) || !(c = j.get("codec")) || c->kind != Json::Str ||
-            !parse_segments(j.get("segments"), ps) || !parse_chunks(j.get("chunks"), pc) ||
-            v != version || wr != w)
-            return DTE_ERR_CORRUPT;
-        if (w == 0) {
-            segs = ps;
-            codec = c->str;
-        } else {
-            if (c->str != codec || ps.size() != segs.size()) return DTE_ERR_ARG;
-            for (size_t i = 0; i < ps.size(); ++i)
-                if (ps[i].name != segs[i].name || ps[i].begin != segs[i].begin ||
-                    ps[i].numel != segs[i].numel)
-                    return DTE_ERR_ARG;
-        }
-        int64_t sum = 0;
-        for (const ChunkMeta& m : pc) sum += m.count;
-        if (sum != e) return DTE_ERR_CORRUPT;
-        entries += e;
-        chunks.insert(chunks.end(), pc.begin(), pc.end());
-    }
-    if (entries == 0) {   // no changed payload anywhere: no new version
-        if (DIR* dd = opendir(vd.c_str())) {
-            while (dirent* de = readdir(dd)) {
-                const std::string nm = de->d_name;
-                if (nm != "." && nm != "..") ::unlink((vd + "/" + nm).c_str());
+    return dte::no_throw([&]() -> dte_status {
+        if (!dir || version < 1 || parent < 0 || parent >= version || nwriters < 1 || nwriters > 4096 ||
+            !committed)
+            return DTE_ERR_ARG;
+        *committed = 0;
+        const std::string d(dir), vd = vdir(d, version);
+        std::vector<Segment> segs;
+        std::vector<ChunkMeta> chunks;
+        std::string codec;
+        int64_t entries = 0;
+        for (int32_t w = 0; w < nwriters; ++w) {
+            std::vector<uint8_t> text;
+            if (!read_file(vd + "/part-" + std::to_string(w) + ".json", text)) return DTE_ERR_IO;
+            Json j;
+            int64_t v = 0, wr = 0, e = 0;
+            std::vector<Segment> ps;
+            std::vector<ChunkMeta> pc;
+            const Json* c = nullptr;
+            if (!parse_json(text, j) || !int_of(j, "version", v) || !int_of(j, "writer", wr) ||
+                !int_of(j, "entries", e) || !(c = j.get("codec")) || c->kind != Json::Str ||
+                !parse_segments(j.get("segments"), ps) || !parse_chunks(j.get("chunks"), pc) ||
+                v != version || wr != w)
+                return DTE_ERR_CORRUPT;
+            if (w == 0) {
+                segs = ps;
+                codec = c->str;
+            } else {
+                if (c->str != codec || ps.size() != segs.size()) return DTE_ERR_ARG;
+                for (size_t i = 0; i < ps.size(); ++i)
+                    if (ps[i].name != segs[i].name || ps[i].begin != segs[i].begin ||
+                        ps[i].numel != segs[i].numel)
+                        return DTE_ERR_ARG;
             }
-            closedir(dd);
+            int64_t sum = 0;
+            for (const ChunkMeta& m : pc) sum += m.count;
+            if (sum != e) return DTE_ERR_CORRUPT;
+            entries += e;
+            chunks.insert(chunks.end(), pc.begin(), pc.end());
         }
-        ::rmdir(vd.c_str());
+        if (entries == 0) {   // no changed payload anywhere: no new version
+            if (DIR* dd = opendir(vd.c_str())) {
+                while (dirent* de = readdir(dd)) {
+                    const std::string nm = de->d_name;
+                    if (nm != "." && nm != "..") ::unlink((vd + "/" + nm).c_str());
+                }
+                closedir(dd);
+            }
+            ::rmdir(vd.c_str());
+            return DTE_OK;
+        }
+        std::sort(chunks.begin(), chunks.end(), [](const ChunkMeta& a, const ChunkMeta& b) {
+            if (a.segment != b.segment) return a.segment < b.segment;
+            return a.writer != b.writer ? a.writer < b.writer : a.first < b.first;
+        });
+        std::string s = "{\"format\": \"dte-delta-1\", \"version\": " + std::to_string(version) +
+                        ", \"parent\": " + std::to_string(parent) + ", \"codec\": \"" + codec +
+                        "\", \"writers\": " + std::to_string(nwriters) +
+                        ", \"entries\": " + std::to_string(entries) + ",\n\"segments\": " +
+                        segments_json(segs) + ",\n\"chunks\": [";
+        for (size_t i = 0; i < chunks.size(); ++i) s += (i ? ",\n  " : "\n  ") + chunk_json(chunks[i]);
+        s += "]}\n";
+        if (!write_atomic(vd + "/manifest.json", s.data(), s.size())) return DTE_ERR_IO;
+        const std::string latest = std::to_string(version) + "\n";
+        if (!write_atomic(d + "/LATEST", latest.data(), latest.size())) return DTE_ERR_IO;
+        *committed = 1;
         return DTE_OK;
-    }
-    std::sort(chunks.begin(), chunks.end(), [](const ChunkMeta& a, const ChunkMeta& b) {
-        if (a.segment != b.segment) return a.segment < b.segment;
-        return a.writer != b.writer ? a.writer < b.writer : a.first < b.first;
     });
-    std::string s = "{\"format\": \"dte-delta-1\", \"version\": " + std::to_string(version) +
-                    ", \"parent\": " + std::to_string(parent) + ", \"codec\": \"" + codec +
-                    "\", \"writers\": " + std::to_string(nwriters) +
-                    ", \"entries\": " + std::to_string(entries) + ",\n\"segments\": " +
-                    segments_json(segs) + ",\n\"chunks\": [";
-    for (size_t i = 0; i < chunks.size(); ++i) s += (i ? ",\n  " : "\n  ") + chunk_json(chunks[i]);
-    s += "]}\n";
-    if (!write_atomic(vd + "/manifest.json", s.data(), s.size())) return DTE_ERR_IO;
-    const std::string latest = std::to_string(version) + "\n";
-    if (!write_atomic(d + "/LATEST", latest.data(), latest.size())) return DTE_ERR_IO;
-    *committed = 1;
-    return DTE_OK;
 }
 
 dte_status dte_store_latest(const char* dir, int64_t* version)
 {
-    if (!dir || !version) return DTE_ERR_ARG;
-    *version = 0;
-    std::vector<uint8_t> text;
-    if (!read_file(std::string(dir) + "/LATEST", text)) return DTE_OK;
-    const std::string t(text.begin(), text.end());
-    char* q = nullptr;
-    const long long v = std::strtoll(t.c_str(), &q, 10);
-    if (q == t.c_str() || v < 1) return DTE_ERR_CORRUPT;
-    *version = v;
-    return DTE_OK;
+    return dte::no_throw([&]() -> dte_status {
+        if (!dir || !version) return DTE_ERR_ARG;
+        *version = 0;
+        std::vector<uint8_t> text;
+        if (!read_file(std::string(dir) + "/LATEST", text)) return DTE_OK;
+        const std::string t(text.begin(), text.end());
+        char* q = nullptr;
+        const long long v = std::strtoll(t.c_str(), &q, 10);
+        if (q == t.c_str() || v < 1) return DTE_ERR_CORRUPT;
+        *version = v;
+        return DTE_OK;
+    });
 }
 
 dte_status dte_store_chain(const char* dir, int64_t base, int64_t latest, int64_t* out, int32_t max,
                            int32_t* n)
 {
-    if (!dir || !n || base < 0 || latest < base || max < 0 || (max > 0 && !out)) return DTE_ERR_ARG;
-    *n = 0;
-    std::vector<int64_t> chain;
-    int64_t v = latest;
-    while (v != base) {
-        if (v < base || v == 0) return DTE_ERR_CHAIN;
-        if ((int64_t)chain.size() >= max) return DTE_ERR_ARG;
-        Manifest m;
-        const dte_status st = load_manifest(dir, v, m);
-        if (st != DTE_OK) return st;
-        chain.push_back(v);
-        if (m.parent >= v) return DTE_ERR_CORRUPT;
-        v = m.parent;
-    }
-    std::reverse(chain.begin(), chain.end());
-    for (size_t i = 0; i < chain.size(); ++i) out[i] = chain[i];
-    *n = (int32_t)chain.size();
-    return DTE_OK;
+    return dte::no_throw([&]() -> dte_status {
+        if (!dir || !n || base < 0 || latest < base || max < 0 || (max > 0 && !out)) return DTE_ERR_ARG;
+        *n = 0;
+        std::vector<int64_t> chain;
+        int64_t v = latest;
+        while (v != base) {
+            if (v < base || v == 0) return DTE_ERR_CHAIN;
+            if ((int64_t)chain.size() >= max) return DTE_ERR_ARG;
+            Manifest m;
+            const dte_status st = load_manifest(dir, v, m);
+            if (st != DTE_OK) return st;
+            chain.push_back(v);
+            if (m.parent >= v) return DTE_ERR_CORRUPT;
+            v = m.parent;
+        }
+        std::reverse(chain.begin(), chain.end());
+        for (size_t i = 0; i < chain.size(); ++i) out[i] = chain[i];
+        *n = (int32_t)chain.size();
+        return DTE_OK;
+    });
 }
 
 
@@ -1299,101 +1329,105 @@ dte_status dte_store_read_host(const char* dir, int64_t version, int64_t base, i
                                uint16_t* val, int64_t capacity, int64_t* count, int32_t threads,
                                dte_store_stats* stats)
 {
-    if (!dir || version < 1 || base < 0 || capacity < 0 || (capacity > 0 && (!idx || !val)) || !count ||
-        threads < 1 || threads > 64)
-        return DTE_ERR_ARG;
-    Manifest m;
-    const dte_status st = load_manifest(dir, version, m);
-    if (st != DTE_OK) return st;
-    if (m.parent != base) return DTE_ERR_CHAIN;
-    *count = m.entries;
-    const dte_status rs = read_chunks(dir, m, threads, [&](size_t k, const uint32_t* local,
-                                                           const uint16_t* v) {
-        const ChunkMeta& c = m.chunks[k];
-        const int64_t at = m.offset[k];
-        const int64_t b = m.segs[c.segment].begin;
-        for (int64_t i = 0; i < c.count && at + i < capacity; ++i) {
-            idx[at + i] = b + (int64_t)local[i];
-            val[at + i] = v[i];
-        }
+    return dte::no_throw([&]() -> dte_status {
+        if (!dir || version < 1 || base < 0 || capacity < 0 || (capacity > 0 && (!idx || !val)) || !count ||
+            threads < 1 || threads > 64)
+            return DTE_ERR_ARG;
+        Manifest m;
+        const dte_status st = load_manifest(dir, version, m);
+        if (st != DTE_OK) return st;
+        if (m.parent != base) return DTE_ERR_CHAIN;
+        *count = m.entries;
+        const dte_status rs = read_chunks(dir, m, threads, [&](size_t k, const uint32_t* local,
+                                                               const uint16_t* v) {
+            const ChunkMeta& c = m.chunks[k];
+            const int64_t at = m.offset[k];
+            const int64_t b = m.segs[c.segment].begin;
+            for (int64_t i = 0; i < c.count && at + i < capacity; ++i) {
+                idx[at + i] = b + (int64_t)local[i];
+                val[at + i] = v[i];
+            }
+            return DTE_OK;
+        });
+        if (rs != DTE_OK) return rs;
+        read_stats(stats, m);
         return DTE_OK;
     });
-    if (rs != DTE_OK) return rs;
-    read_stats(stats, m);
-    return DTE_OK;
 }
 
 dte_status dte_store_read_device(const char* dir, int64_t version, int64_t base, int64_t* idx,
                                  uint16_t* val, int64_t capacity, int64_t* count, int32_t threads,
                                  dte_store_stats* stats, void* stream)
 {
-    if (!dir || version < 1 || base < 0 || capacity < 0 || (capacity > 0 && (!idx || !val)) || !count ||
-        threads < 1 || threads > 64)
-        return DTE_ERR_ARG;
-    Manifest m;
-    dte_status st = load_manifest(dir, version, m);
-    if (st != DTE_OK) return st;
-    if (m.parent != base) return DTE_ERR_CHAIN;
-    *count = m.entries;
-    const int64_t n = std::min(m.entries, capacity);
-    const hipStream_t s = (hipStream_t)stream;
-    // chunk table: first entry and segment base of every chunk that fits
-    std::vector<int64_t> first, cbase;
-    for (size_t k = 0; k < m.chunks.size() && m.offset[k] < n; ++k) {
-        first.push_back(m.offset[k]);
-        cbase.push_back(m.segs[m.chunks[k].segment].begin);
-    }
-    const int32_t nchunk = (int32_t)first.size();
-    int64_t biggest = 1;
-    for (const ChunkMeta& c : m.chunks) biggest = std::max(biggest, c.count);
-    DevBuf dlocal, dfirst, dbase;
-    if (!dlocal.alloc((size_t)std::max<int64_t>(n, 1) * 4) || !dfirst.alloc(first.size() * 8) ||
-        !dbase.alloc(cbase.size() * 8))
-        return DTE_ERR_HIP;
-    uint32_t* loc = static_cast<uint32_t*>(dlocal.p);
-    Ring ring(threads + 2, biggest);
-    if (!ring.ok()) return DTE_ERR_HIP;
-    std::mutex copy_mutex;   // one copier at a time on the stream
-    int device = 0;
-    if (hipGetDevice(&device) != hipSuccess) return DTE_ERR_HIP;
-    st = read_chunks(dir, m, threads, [&](size_t k, const uint32_t* local, const uint16_t* v) {
-        const int64_t at = m.offset[k];
-        if (at >= n) return DTE_OK;
-        const int64_t c = std::min(m.chunks[k].count, n - at);
-        const int slot = ring.acquire();
-        std::memcpy(ring.local(slot), local, (size_t)c * 4);
-        std::memcpy(ring.val(slot), v, (size_t)c * 2);
-        dte_status r = DTE_OK;
-        {
-            std::lock_guard<std::mutex> g(copy_mutex);
-            // pool threads start on device 0: use the caller's device
-            if (hipSetDevice(device) != hipSuccess ||
-                hipMemcpyAsync(loc + at, ring.local(slot), (size_t)c * 4, hipMemcpyHostToDevice, s) !=
-                    hipSuccess ||
-                hipMemcpyAsync(val + at, ring.val(slot), (size_t)c * 2, hipMemcpyHostToDevice, s) !=
-                    hipSuccess ||
-                hipStreamSynchronize(s) != hipSuccess)
-                r = DTE_ERR_HIP;
+    return dte::no_throw([&]() -> dte_status {
+        if (!dir || version < 1 || base < 0 || capacity < 0 || (capacity > 0 && (!idx || !val)) || !count ||
+            threads < 1 || threads > 64)
+            return DTE_ERR_ARG;
+        Manifest m;
+        dte_status st = load_manifest(dir, version, m);
+        if (st != DTE_OK) return st;
+        if (m.parent != base) return DTE_ERR_CHAIN;
+        *count = m.entries;
+        const int64_t n = std::min(m.entries, capacity);
+        const hipStream_t s = (hipStream_t)stream;
+        // chunk table: first entry and segment base of every chunk that fits
+        std::vector<int64_t> first, cbase;
+        for (size_t k = 0; k < m.chunks.size() && m.offset[k] < n; ++k) {
+            first.push_back(m.offset[k]);
+            cbase.push_back(m.segs[m.chunks[k].segment].begin);
         }
-        ring.release(slot);
-        return r;
-    });
-    if (st != DTE_OK) return st;
-    if (n > 0) {
-        if (hipMemcpyAsync(dfirst.p, first.data(), first.size() * 8, hipMemcpyHostToDevice, s) !=
-                hipSuccess ||
-            hipMemcpyAsync(dbase.p, cbase.data(), cbase.size() * 8, hipMemcpyHostToDevice, s) != hipSuccess)
+        const int32_t nchunk = (int32_t)first.size();
+        int64_t biggest = 1;
+        for (const ChunkMeta& c : m.chunks) biggest = std::max(biggest, c.count);
+        DevBuf dlocal, dfirst, dbase;
+        if (!dlocal.alloc((size_t)std::max<int64_t>(n, 1) * 4) || !dfirst.alloc(first.size() * 8) ||
+            !dbase.alloc(cbase.size() * 8))
             return DTE_ERR_HIP;
-        const int64_t want = (n + 255) / 256;
-        const int64_t cap = (int64_t)device_cus() * 8;
-        hipLaunchKernelGGL(widen_kernel, dim3((unsigned)std::min(want, cap)), dim3(256), 0, s, loc, n,
-                           static_cast<const int64_t*>(dfirst.p), static_cast<const int64_t*>(dbase.p),
-                           nchunk, idx);
-        if (hipGetLastError() != hipSuccess) return DTE_ERR_HIP;
-    }
-    if (hipStreamSynchronize(s) != hipSuccess) return DTE_ERR_HIP;
-    read_stats(stats, m);
-    return DTE_OK;
+        uint32_t* loc = static_cast<uint32_t*>(dlocal.p);
+        Ring ring(threads + 2, biggest);
+        if (!ring.ok()) return DTE_ERR_HIP;
+        std::mutex copy_mutex;   // one copier at a time on the stream
+        int device = 0;
+        if (hipGetDevice(&device) != hipSuccess) return DTE_ERR_HIP;
+        st = read_chunks(dir, m, threads, [&](size_t k, const uint32_t* local, const uint16_t* v) {
+            const int64_t at = m.offset[k];
+            if (at >= n) return DTE_OK;
+            const int64_t c = std::min(m.chunks[k].count, n - at);
+            const int slot = ring.acquire();
+            std::memcpy(ring.local(slot), local, (size_t)c * 4);
+            std::memcpy(ring.val(slot), v, (size_t)c * 2);
+            dte_status r = DTE_OK;
+            {
+                std::lock_guard<std::mutex> g(copy_mutex);
+                // pool threads start on device 0: use the caller's device
+                if (hipSetDevice(device) != hipSuccess ||
+                    hipMemcpyAsync(loc + at, ring.local(slot), (size_t)c * 4, hipMemcpyHostToDevice, s) !=
+                        hipSuccess ||
+                    hipMemcpyAsync(val + at, ring.val(slot), (size_t)c * 2, hipMemcpyHostToDevice, s) !=
+                        hipSuccess ||
+                    hipStreamSynchronize(s) != hipSuccess)
+                    r = DTE_ERR_HIP;
+            }
+            ring.release(slot);
+            return r;
+        });
+        if (st != DTE_OK) return st;
+        if (n > 0) {
+            if (hipMemcpyAsync(dfirst.p, first.data(), first.size() * 8, hipMemcpyHostToDevice, s) !=
+                    hipSuccess ||
+                hipMemcpyAsync(dbase.p, cbase.data(), cbase.size() * 8, hipMemcpyHostToDevice, s) != hipSuccess)
+                return DTE_ERR_HIP;
+            const int64_t want = (n + 255) / 256;
+            const int64_t cap = (int64_t)device_cus() * 8;
+            hipLaunchKernelGGL(widen_kernel, dim3((unsigned)std::min(want, cap)), dim3(256), 0, s, loc, n,
+                               static_cast<const int64_t*>(dfirst.p), static_cast<const int64_t*>(dbase.p),
+                               nchunk, idx);
+            if (hipGetLastError() != hipSuccess) return DTE_ERR_HIP;
+        }
+        if (hipStreamSynchronize(s) != hipSuccess) return DTE_ERR_HIP;
+        read_stats(stats, m);
+        return DTE_OK;
+    });
 }
 
 }  // extern "C"

@@ -90,6 +90,17 @@ def test_argument_errors_and_empty_calls():
     assert "ERR_PLAN" in B.dte_status_string(B.DTE_ERR_PLAN)
 
 
+def test_every_status_code_has_its_own_name():
+    codes = [B.DTE_OK, B.DTE_ERR_ARG, B.DTE_ERR_PLAN, B.DTE_ERR_CAPACITY, B.DTE_ERR_HIP,
+             B.DTE_ERR_IO, B.DTE_ERR_CORRUPT, B.DTE_ERR_CHAIN, B.DTE_ERR_UNSUPPORTED,
+             B.DTE_ERR_HOST]
+    assert codes == list(range(10))
+    names = [B.dte_status_string(c) for c in codes]
+    assert len(set(names)) == len(names)
+    assert names[0] == "DTE_OK" and names[9].startswith("DTE_ERR_HOST")
+    assert B.dte_status_string(10) == "unknown dte_status"
+
+
 def _create_status(spec, segs=None, ops=None, numel=None):
     segs = segs if segs is not None else spec.c_segments()
     ops = ops if ops is not None else spec.c_ops()

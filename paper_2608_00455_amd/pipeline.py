@@ -17,6 +17,22 @@ from . import binding as B
 from .layouts import PlanSpec, build_spec
 
 
+def check_buffer(t, n, dtype, device, name):
+    """The library takes raw addresses and element counts, so a buffer of
+    the wrong type, layout, device or length would be read or written out
+    of bounds: refuse it here."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s: expected a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise ValueError("%s: dtype %s, expected %s" % (name, t.dtype, dtype))
+    if t.device != device:
+        raise ValueError("%s: on %s, expected %s" % (name, t.device, device))
+    if not t.is_contiguous():
+        raise ValueError("%s: not contiguous" % name)
+    if t.numel() < n:
+        raise ValueError("%s: %d elements, %d needed" % (name, t.numel(), n))
+
+
 def _stream(stream=None) -> int:
     s = stream if stream is not None else torch.cuda.current_stream()
     return s.cuda_stream
@@ -65,6 +81,10 @@ class DeltaPipeline:
         if shards is None:
             shards = [torch.zeros(max(1, n), dtype=torch.int16, device=self.device)
                       for n in spec.rank_numel]
+        if len(shards) != R:
+            raise ValueError("shards: %d buffers for %d receiver ranks" % (len(shards), R))
+        for r, (t, n) in enumerate(zip(shards, spec.rank_numel)):
+            check_buffer(t, n, torch.int16, self.idx.device, "shards[%d]" % r)
         self.shards = shards
         self.workspace = None
         if ordered:
@@ -77,8 +97,20 @@ class DeltaPipeline:
         with torch.cuda.stream(stream) if stream is not None else _null():
             self.cursor.zero_()
 
+    def _check_state(self, p, m, v, n, out_prev=None) -> int:
+        """Element count of the call (all of p when n is None), after
+        checking p, m, v (and out_prev) for it."""
+        if not isinstance(p, torch.Tensor):
+            raise TypeError("p: expected a torch.Tensor")
+        n = p.numel() if n is None else int(n)
+        for t, name in ((p, "p"), (m, "m"), (v, "v")):
+            check_buffer(t, n, torch.float32, self.idx.device, name)
+        if out_prev is not None:
+            check_buffer(out_prev, n, torch.float32, self.idx.device, "out_prev")
+        return n
+
     def extract(self, p, m, v, hp, n=None, index_base=0, out_prev=None, stream=None):
-        n = p.numel() if n is None else n
+        n = self._check_state(p, m, v, n, out_prev)
         prev = out_prev.data_ptr() if out_prev is not None else 0
         if self.ordered:
             B.dte_extract_delta_ordered(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, index_base,
@@ -113,7 +145,7 @@ class DeltaPipeline:
     def extract_remap(self, p, m, v, hp, n=None, index_base=0, stream=None):
         """Changed entries routed straight into the buckets (adds to
         rank_count and to the cursor; clear both first, see step_fused)."""
-        n = p.numel() if n is None else n
+        n = self._check_state(p, m, v, n)
         B.dte_extract_remap(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, index_base, hp,
                             self.plan.handle, [t.data_ptr() for t in self.off],
                             [t.data_ptr() for t in self.rval], self.rank_capacity,

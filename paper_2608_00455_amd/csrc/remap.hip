@@ -10,15 +10,16 @@
 // receiver view (eq. receiver_local_remapping).
 //
 // Work unit: a wave takes 512 consecutive entries (8 per lane) into
-// registers.  Extract emits local ascending runs, so a chunk usually lies in
+// registers, and keeps them there from counting to writing.  Extract emits local ascending runs, so a chunk usually lies in
 // one segment: then each operation of the segment is loaded once (into
 // scalar registers) and tested against all eight slots, one ballot per slot.
 // Chunks that span segments route slot by slot, lanes grouped by segment.
-// Each block owns a contiguous slice of the entries; pass 1 counts the
-// slice's outputs per rank, one atomicAdd per touched rank and block
-// reserves bucket space, pass 2 recomputes and writes (offset, value) at
-// the reserved positions (a few atomics per block: same-address atomics
-// serialise at the memory side, so they are kept out of the inner loops).
+// Each block owns a contiguous slice of the entries, taken 2048 at a time
+// (one chunk per wave): count the outputs per rank, reserve bucket space
+// with one atomicAdd per touched rank, recompute and write (offset, value)
+// at the reserved positions from the same registers (a few atomics per
+// block: same-address atomics serialise at the memory side, so they are
+// kept out of the inner loops).
 //
 // Apply: shard[off] = val; each lane keeps eight independent
 // load-then-store chains in flight (the scattered 2-byte stores are
@@ -44,6 +45,7 @@ __global__ void zero_i64_kernel(int64_t* p, int64_t n)
 constexpr int kWaves = kBlock / 64;
 constexpr int kRemapSlots = 8;                     // entries per lane per chunk
 constexpr int kChunk = 64 * kRemapSlots;           // entries per wave per chunk
+constexpr int64_t kGroup = (int64_t)kWaves * kChunk;  // entries per block per reservation
 // Slice size and grid of remap: many small slices balance the uneven cost
 // of routing (segments differ in operation count) better than one slice
 // per resident block, but every block costs a reservation round trip, so a
@@ -53,7 +55,7 @@ constexpr int kChunk = 64 * kRemapSlots;           // entries per wave per chunk
 // once.
 constexpr int64_t kBlockEntries = 4096;
 constexpr int64_t kMinBlockEntries = 64;
-constexpr int kRemapBlocksPerCU = 64;
+constexpr int kRemapBlocksPerCU = 128;
 constexpr int kRemapFillPerCU = 5;                 // blocks per CU that keep the chip busy
 
 // Whole chunk inside one segment of kNd dimensions: each
@@ -103,25 +105,38 @@ __device__ __forceinline__ void route_chunk_in(const PlanView& pl, const RankSli
     route_chunk<kWrite, kNd>(pl, out, lane, sg, x, y, u, runv, basev);
 }
 
-// Route the chunk of entries [c0, c1): counting pass (kWrite == false) or
-// writing pass.  Wave-uniform.
-template <bool kWrite>
-__device__ __forceinline__ void route_range(const PlanView& pl, const RankSlice& out, int lane,
-                                            const int64_t* __restrict__ idx,
-                                            const uint16_t* __restrict__ val, int64_t c0,
-                                            int64_t c1, int& runv, int64_t basev, SegInfo& cache)
+// Load the chunk of entries [c0, c1) (empty when c0 >= c1) into eight
+// slots per lane; offsets outside the plan become -1 (ignored).
+__device__ __forceinline__ void load_chunk(const PlanView& pl, const int64_t* __restrict__ idx,
+                                           const uint16_t* __restrict__ val, int64_t c0,
+                                           int64_t c1, int lane, int64_t* x, uint16_t* y)
 {
-    int64_t x[kRemapSlots];
-    uint16_t y[kRemapSlots];
+    if (c0 >= c1) {
+#pragma unroll
+        for (int j = 0; j < kRemapSlots; ++j) {
+            x[j] = -1;
+            y[j] = 0;
+        }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < kRemapSlots; ++j) {     // all loads of the chunk in flight
         int64_t e = c0 + j * 64 + lane;
         const bool ok = e < c1;
         e = ok ? e : c0;
         x[j] = idx[e];
-        y[j] = kWrite ? val[e] : (uint16_t)0;
+        y[j] = val[e];
         x[j] = (ok && x[j] >= 0 && x[j] < pl.total) ? x[j] : -1;   // outside: ignored
     }
+}
+
+// Route a loaded chunk: counting pass (kWrite == false) or writing pass.
+// Wave-uniform.
+template <bool kWrite>
+__device__ __forceinline__ void route_loaded(const PlanView& pl, const RankSlice& out, int lane,
+                                             const int64_t* x, const uint16_t* y, int& runv,
+                                             int64_t basev, SegInfo& cache)
+{
     // does one segment hold the whole chunk?
     uint64_t any = 0;
     int64_t i0 = 0;
@@ -152,13 +167,14 @@ __device__ __forceinline__ void route_range(const PlanView& pl, const RankSlice&
     }
 }
 
-// G blocks take part (see kBlockEntries).  Block b < G
-// owns entries [total b / G, total (b+1) / G), both ends rounded down to
-// whole chunks when the delta has at least four chunks per block (the last
-// block ends at total); its waves take every fourth chunk.  Pass 1 counts
-// per rank, the block reserves bucket space with one atomicAdd per rank,
-// pass 2 writes: wave w of the block writes after the outputs of waves
-// 0..w-1, each wave in its own chunk order.
+// G blocks take part (see kBlockEntries).  Block b < G owns entries
+// [total b / G, total (b+1) / G), both ends rounded down to whole groups
+// (kGroup: one chunk per wave) when the delta has at least two groups per
+// block, else to whole chunks when it has four chunks per block (the last
+// block ends at total).  Per group, each wave loads its chunk into
+// registers once, counts its outputs per rank, the block reserves bucket
+// space with one atomicAdd per touched rank, and each wave writes from the
+// same registers after the outputs of waves 0..w-1.
 __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_t* __restrict__ idx,
                                                        const uint16_t* __restrict__ val,
                                                        const int64_t* __restrict__ count,
@@ -174,9 +190,10 @@ __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_
     if (total < 0) total = 0;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    // slices start on chunk boundaries when each block gets several chunks:
-    // extract flushes whole 1024-entry runs, so a chunk then lies in one run
-    // (usually one segment); small deltas are split evenly instead
+    // slices start on group (else chunk) boundaries when each block gets
+    // several: no group is left partly empty, and since extract flushes
+    // whole 1024-entry runs a chunk then lies in one run (usually one
+    // segment); small deltas are split evenly instead
     // blocks in use: about kBlockEntries entries each, more (at least
     // kMinBlockEntries each) up to `fill` blocks, at most the grid
     int64_t g = (total + kBlockEntries - 1) / kBlockEntries;
@@ -185,36 +202,38 @@ __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_
     g = g > gfill ? g : gfill;
     g = g < 1 ? 1 : (g > (int64_t)gridDim.x ? (int64_t)gridDim.x : g);
     if ((int64_t)blockIdx.x >= g) return;
-    const int64_t align = total >= g * 4 * kChunk ? kChunk : 1;
+    const int64_t align = total >= g * 2 * kGroup ? kGroup : (total >= g * 4 * kChunk ? kChunk : 1);
     const int64_t lo = total * blockIdx.x / g / align * align;
     const int64_t hi = blockIdx.x + 1 == g ? total : total * (blockIdx.x + 1) / g / align * align;
     SegInfo cache{};
-
-    int runv = 0;                                       // lane r: outputs for rank first + r
-    for (int64_t c0 = lo + (int64_t)wave * kChunk; c0 < hi; c0 += (int64_t)kWaves * kChunk)
-        route_range<false>(pl, out, lane, idx, val, c0, c0 + kChunk < hi ? c0 + kChunk : hi, runv,
-                           0, cache);
-    if (lane < kRanksPerLaunch) s_cnt[wave][lane] = lane < out.count ? runv : 0;
-    __syncthreads();
-    if (wave == 0 && lane < out.count) {
-        int64_t n = 0;
+    for (int64_t g0 = lo; g0 < hi; g0 += kGroup) {     // block-uniform trip count
+        int64_t x[kRemapSlots];
+        uint16_t y[kRemapSlots];
+        const int64_t c0 = g0 + (int64_t)wave * kChunk;
+        load_chunk(pl, idx, val, c0, c0 + kChunk < hi ? c0 + kChunk : hi, lane, x, y);
+        int runv = 0;                                   // lane r: outputs for rank first + r
+        route_loaded<false>(pl, out, lane, x, y, runv, 0, cache);
+        if (lane < kRanksPerLaunch) s_cnt[wave][lane] = lane < out.count ? runv : 0;
+        __syncthreads();
+        if (wave == 0 && lane < out.count) {
+            int64_t n = 0;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) n += s_cnt[w][lane];
-        s_base[lane] = n > 0 ? (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(
-                                                      &rank_count[out.first + lane]),
-                                                  (unsigned long long)n)
-                             : 0;
+            for (int w = 0; w < kWaves; ++w) n += s_cnt[w][lane];
+            s_base[lane] = n > 0 ? (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(
+                                                          &rank_count[out.first + lane]),
+                                                      (unsigned long long)n)
+                                 : 0;
+        }
+        __syncthreads();
+        int64_t basev = 0;
+        if (lane < out.count) {
+            basev = s_base[lane];
+            for (int w = 0; w < wave; ++w) basev += s_cnt[w][lane];
+        }
+        runv = 0;
+        route_loaded<true>(pl, out, lane, x, y, runv, basev, cache);
+        __syncthreads();                                // s_cnt and s_base are reused
     }
-    __syncthreads();
-    int64_t basev = 0;
-    if (lane < out.count) {
-        basev = s_base[lane];
-        for (int w = 0; w < wave; ++w) basev += s_cnt[w][lane];
-    }
-    runv = 0;
-    for (int64_t c0 = lo + (int64_t)wave * kChunk; c0 < hi; c0 += (int64_t)kWaves * kChunk)
-        route_range<true>(pl, out, lane, idx, val, c0, c0 + kChunk < hi ? c0 + kChunk : hi, runv,
-                          basev, cache);
 }
 
 constexpr int kApplyUnroll = 8;

@@ -81,3 +81,69 @@ def test_remap_and_apply_with_capped_grid():
         expect = torch.zeros_like(shards[r])
         expect[want] = value_of(want + r * HALF * COLS)
         assert torch.equal(shards[r], expect), r
+
+
+def test_remap_and_apply_on_the_largest_segment():
+    """A 65536 x 65535 matrix (4,294,901,760 elements, just under the
+    2^32 limit of a segment): segment-local indices near the top of their
+    32-bit range, the first and last elements and both sides of the row
+    split, 50 M random entries in all."""
+    rows, cols = 65536, 65535
+    half = rows // 2
+    total = rows * cols
+    print("case: largest segment, %d elements" % total, flush=True)
+    sys.stdout.flush()
+    dev = torch.device("cuda")
+    g = torch.Generator(device=dev)
+    g.manual_seed(26080456)
+    edges = torch.tensor([0, 1, cols - 1, half * cols - 1, half * cols, total - cols, total - 2,
+                          total - 1], dtype=torch.int64, device=dev)
+    rnd = torch.randint(0, total, (50_000_000,), generator=g, device=dev, dtype=torch.int64)
+    idx = torch.unique(torch.cat([rnd, edges]))
+    idx = idx[torch.randperm(idx.numel(), generator=g, device=dev)].contiguous()
+    m = idx.numel()
+    val = value_of(idx)
+    seg = B.dte_segment()
+    seg.flat_begin, seg.ndim = 0, 2
+    seg.shape[0], seg.shape[1] = rows, cols
+    ops = []
+    for r in range(2):
+        o = B.dte_op()
+        o.segment, o.rank, o.dst_base = 0, r, 0
+        o.src_origin[0], o.src_origin[1] = r * half, 0
+        o.extent[0], o.extent[1] = half, cols
+        o.dst_origin[0], o.dst_origin[1] = 0, 0
+        o.dst_shape[0], o.dst_shape[1] = half, cols
+        ops.append(o)
+    h = B.dte_plan_create([seg], ops, 2, [half * cols, half * cols])
+    count = torch.tensor([m], dtype=torch.int64, device=dev)
+    off = [torch.empty(m, dtype=torch.int64, device=dev) for _ in range(2)]
+    rval = [torch.empty(m, dtype=torch.int16, device=dev) for _ in range(2)]
+    rank_count = torch.zeros(2, dtype=torch.int64, device=dev)
+    shards = [torch.zeros(half * cols, dtype=torch.int16, device=dev) for _ in range(2)]
+    try:
+        s = torch.cuda.current_stream().cuda_stream
+        B.dte_remap(h, idx.data_ptr(), val.data_ptr(), count.data_ptr(), m,
+                    [t.data_ptr() for t in off], [t.data_ptr() for t in rval], [m, m],
+                    rank_count.data_ptr(), s)
+        B.dte_apply(h, [t.data_ptr() for t in shards], [t.data_ptr() for t in off],
+                    [t.data_ptr() for t in rval], rank_count.data_ptr(), [m, m], s)
+        torch.cuda.synchronize()
+    finally:
+        B.dte_plan_destroy(h)
+    low = idx < half * cols
+    want_count = [int(low.sum().item()), m - int(low.sum().item())]
+    assert rank_count.cpu().tolist() == want_count
+    for r in range(2):
+        k = want_count[r]
+        mine, order = torch.sort(off[r][:k])
+        want = torch.sort(idx[low if r == 0 else ~low] - r * half * cols).values
+        assert torch.equal(mine, want), r
+        assert torch.equal(rval[r][:k][order], value_of(want + r * half * cols)), r
+        expect = torch.zeros_like(shards[r])
+        expect[want] = value_of(want + r * half * cols)
+        assert torch.equal(shards[r], expect), r
+        del expect
+    # the extremes went where they belong
+    last = shards[1][half * cols - 1].item()
+    assert last == int(value_of(torch.tensor([total - 1]))[0])

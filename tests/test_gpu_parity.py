@@ -194,9 +194,11 @@ def test_ragged_misaligned_and_appended_ranges():
     pipe.close()
 
 
+@pytest.mark.parametrize("base", [1000, (1 << 40) + 7])
 @pytest.mark.parametrize("order", [W.ORDER_FOLDED, W.ORDER_LITERAL])
-def test_special_values(order):
-    say("case: special values", order)
+def test_special_values(order, base):
+    """index_base 2^40 + 7: offsets far beyond 32 bits come out exact."""
+    say("case: special values", order, base)
     rng = np.random.default_rng(3)
     n = 5000
     p = (rng.standard_normal(n) * 0.02).astype(np.float32)
@@ -215,12 +217,12 @@ def test_special_values(order):
     for lr in (1e-6, 1e-4, 3e-1):
         hp = W.StepHP(lr=lr, order=order)
         sc = ocore.derive_scalars(hp)
-        want_idx, want_val, want_ph = ocore.detect(p, m, v, sc, 1000)
+        want_idx, want_val, want_ph = ocore.detect(p, m, v, sc, base)
         spec = layouts.build_spec(W.scaled_dense(layers=1, tp=2))
         pipe = DeltaPipeline(spec, capacity=n)
         prev = torch.empty(n, dtype=torch.float32, device="cuda")
         pipe.reset()
-        pipe.extract(dev(p), dev(m), dev(v), hp, index_base=1000, out_prev=prev)
+        pipe.extract(dev(p), dev(m), dev(v), hp, index_base=base, out_prev=prev)
         sync()
         idx, val, total = pipe.delta()
         assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val), lr
@@ -230,7 +232,7 @@ def test_special_values(order):
         assert np.array_equal(got_ph.view(np.uint32)[~nan], want_ph.view(np.uint32)[~nan])
         # and through the "unchanged" proof (no theta_hat requested)
         pipe.reset()
-        pipe.extract(dev(p), dev(m), dev(v), hp, index_base=1000)
+        pipe.extract(dev(p), dev(m), dev(v), hp, index_base=base)
         sync()
         idx, val, total = pipe.delta()
         assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val), lr

@@ -15,7 +15,7 @@ def pytest_configure(config):
 
 def pytest_collection_modifyitems(config, items):
     # GPU tests cannot run without a visible GPU: skip them with a reason
-    # (the round-end GPU run selects them with -m gpu on a GPU machine).
+    # (on a machine with an MI355X, select them with -m gpu).
     try:
         import torch
         have_gpu = torch.cuda.is_available()

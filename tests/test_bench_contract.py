@@ -1,15 +1,20 @@
 """Host-side checks of bench.py: the one-GPU rule and the traffic record
 lookup (no GPU needed)."""
+import glob
 import hashlib
 import json
 import os
 import subprocess
 import sys
 
+import pytest
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 
 import bench  # noqa: E402
+
+RECORDS = sorted(glob.glob(os.path.join(ROOT, "profiles", "extract_*_traffic.json")))
 
 
 def test_more_than_one_gpu_is_refused_with_a_message():
@@ -20,11 +25,16 @@ def test_more_than_one_gpu_is_refused_with_a_message():
     assert r.stdout == ""
 
 
-def test_traffic_record_lookup():
-    path = os.path.join(ROOT, "profiles", "extract_qwen3_8b_tp4_traffic.json")
+def test_the_benchmark_workload_has_a_traffic_record():
+    assert os.path.join(ROOT, "profiles", "extract_qwen3_8b_tp4_traffic.json") in RECORDS
+
+
+@pytest.mark.parametrize("path", RECORDS, ids=[os.path.basename(p) for p in RECORDS])
+def test_traffic_record_lookup(path):
     rec = json.load(open(path))
+    workload = os.path.basename(path)[len("extract_"):-len("_traffic.json")]
     src = os.path.join(ROOT, rec["kernel_source"])
-    got = bench.measured_traffic("qwen3_8b_tp4", "extract", rec["mode"])
+    got = bench.measured_traffic(workload, "extract", rec["mode"])
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["kernel_source_sha256"]:
         # the kernel changed since the counters were taken: bench reports null
         assert got is None
@@ -36,8 +46,7 @@ def test_traffic_record_lookup():
              sum(rec["write_size_kib_per_call"].values()) * 1024 * cal["write_factor"])
     assert abs(total - got) < 1.0
     # within a fraction of a percent of extract's algorithmic bytes 12 N + 10 M
-    algorithmic = 12 * 8190735360 + 10 * 25978374
-    assert 1.0 <= got / algorithmic < 1.01
+    assert 1.0 <= got / rec["algorithmic_bytes_per_launch"] < 1.01
 
 
 def test_traffic_is_withheld_for_another_mode_or_workload():

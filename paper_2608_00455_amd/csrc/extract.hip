@@ -58,6 +58,11 @@ constexpr int kWaveTile = 64 * kSlots;        // 2048 elements per wave tile
 constexpr int kWaveStage = 1024;              // staged output entries per wave (6 bytes each)
 constexpr int kQueue = 256;                   // queued candidates per wave (16 bytes each)
 constexpr int kBlocksPerCU = 3;               // 3 waves per SIMD (VGPR-bound), 40 KB LDS
+// a float4 slot selects up to 4 x 64 elements at once: they must fit an
+// empty candidate queue, and the part left after one flush of the staging
+// area must fit the emptied area
+static_assert(kQueue >= 4 * 64, "a slot's candidates must fit the queue");
+static_assert(kWaveStage >= 4 * 64, "a slot's changed entries must fit after one flush");
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 

@@ -99,11 +99,7 @@ __device__ __forceinline__ uint32_t bf16_bits(float x)
     return (x != x) ? 0x7FC0u : r;
 }
 
-__device__ __forceinline__ int lane_prefix(uint64_t mask)
-{
-    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-}
+using rt::lane_prefix;   // set lanes of the mask below this lane
 
 template <bool kVecLoads>
 __device__ __forceinline__ f32x4 load4(const float* base, int64_t e, int64_t n)

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <memory>
@@ -27,18 +28,20 @@ struct dte_plan {
 
 namespace {
 
+// Compute units of a device, queried once per device (calls may come from
+// several host threads: the cache is atomic; a race only repeats the query).
 int cu_count(int device)
 {
-    static int cache[64] = {0};
+    static std::atomic<int> cache[64];
     if (device < 0 || device >= 64) return 256;
-    if (cache[device] == 0) {
-        int n = 0;
+    int n = cache[device].load(std::memory_order_relaxed);
+    if (n == 0) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) !=
                 hipSuccess || n <= 0)
             n = 256;
-        cache[device] = n;
+        cache[device].store(n, std::memory_order_relaxed);
     }
-    return cache[device];
+    return n;
 }
 
 // The plan's tables live on the device it was created on; the hot calls

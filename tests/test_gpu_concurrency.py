@@ -1,0 +1,73 @@
+"""One transfer plan shared by concurrent calls on two streams (the plan
+is immutable once created, include/dte.h): two different deltas are
+remapped and applied at the same time, each into its own buckets and
+shards, and each result equals the oracle's remap (sec. 3.2.2) and apply
+(sec. 3.3) of its own delta."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from highdim_plan import HighDimSpec
+from oracle import remap as oremap
+from paper_2608_00455_amd import binding as B
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def test_one_plan_shared_by_two_streams():
+    print("case: plan shared by two streams", flush=True)
+    sys.stdout.flush()
+    spec = HighDimSpec()
+    rng = np.random.default_rng(26080455 + 77)
+    h = B.dte_plan_create(spec.c_segments(), spec.c_ops(), spec.nranks, spec.rank_numel)
+    jobs = []
+    try:
+        for k in range(2):
+            idx = np.flatnonzero(rng.random(spec.numel) < (0.2 + 0.3 * k)).astype(np.int64)
+            rng.shuffle(idx)
+            val = rng.integers(0, 1 << 16, idx.size, dtype=np.uint16)
+            old = [np.full(n, 0x1234 + k, np.uint16) for n in spec.rank_numel]
+            cap = [max(1, n) for n in spec.rank_numel]
+            job = dict(idx=idx, val=val, old=old, cap=cap, stream=torch.cuda.Stream(),
+                       d_idx=dev(idx), d_val=dev(val.view(np.int16)),
+                       count=torch.tensor([idx.size], dtype=torch.int64, device="cuda"),
+                       off=[torch.empty(c, dtype=torch.int64, device="cuda") for c in cap],
+                       rval=[torch.empty(c, dtype=torch.int16, device="cuda") for c in cap],
+                       rank_count=torch.zeros(spec.nranks, dtype=torch.int64, device="cuda"),
+                       shards=[dev(x.view(np.int16)) for x in old])
+            jobs.append(job)
+        torch.cuda.synchronize()
+        for _ in range(3):                     # interleaved launches on both streams
+            for job in jobs:
+                with torch.cuda.stream(job["stream"]):
+                    s = job["stream"].cuda_stream
+                    B.dte_remap(h, job["d_idx"].data_ptr(), job["d_val"].data_ptr(),
+                                job["count"].data_ptr(), job["idx"].size,
+                                [t.data_ptr() for t in job["off"]],
+                                [t.data_ptr() for t in job["rval"]], job["cap"],
+                                job["rank_count"].data_ptr(), s)
+                    B.dte_apply(h, [t.data_ptr() for t in job["shards"]],
+                                [t.data_ptr() for t in job["off"]],
+                                [t.data_ptr() for t in job["rval"]],
+                                job["rank_count"].data_ptr(), job["cap"], s)
+        torch.cuda.synchronize()
+    finally:
+        B.dte_plan_destroy(h)
+    for k, job in enumerate(jobs):
+        want = oremap.remap(spec.oracle_plan, job["idx"], job["val"])
+        expect = oremap.apply([x.copy() for x in job["old"]], want)
+        counts = job["rank_count"].cpu().numpy()
+        for r in range(spec.nranks):
+            assert counts[r] == want[r][0].size, (k, r)
+            off = job["off"][r][:counts[r]].cpu().numpy()
+            val = job["rval"][r][:counts[r]].cpu().numpy().view(np.uint16)
+            order = off.argsort(kind="stable")
+            assert np.array_equal(off[order], want[r][0]), (k, r)
+            assert np.array_equal(val[order], want[r][1]), (k, r)
+            assert np.array_equal(job["shards"][r].cpu().numpy().view(np.uint16), expect[r]), (k, r)

@@ -371,8 +371,8 @@ int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 OrderedWorkspace ordered_layout(int64_t capacity)
 {
     OrderedWorkspace w;
-    // every flush but a wave's last holds exactly 1024 entries
-    w.max_runs = capacity / 1024 + dte::kMaxOrderedWaves + 1;
+    // every flush but a wave's last holds exactly kWaveStage entries
+    w.max_runs = capacity / dte::kWaveStage + dte::kMaxOrderedWaves + 1;
     w.ridx = 0;
     w.rval = align256(w.ridx + capacity * (int64_t)sizeof(int64_t));
     w.idx = align256(w.rval + capacity * (int64_t)sizeof(uint16_t));

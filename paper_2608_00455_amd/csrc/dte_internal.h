@@ -100,6 +100,9 @@ struct ExtractParams {
 
 // Largest number of waves one extract call launches in ordered mode.
 constexpr int kMaxOrderedWaves = 16384;
+// Entries a wave stages before it flushes them: every flush but a wave's
+// last holds exactly this many (the ordered workspace is sized with it).
+constexpr int kWaveStage = 1024;
 
 // Launches the extract kernels; *waves receives the number of waves
 // launched (the global wave numbers are 0 .. *waves - 1).

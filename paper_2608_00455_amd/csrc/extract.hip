@@ -55,7 +55,6 @@ constexpr int kWaves = kBlock / 64;
 constexpr int kVec = 8;                       // float4 per lane per array per tile
 constexpr int kSlots = 4 * kVec;              // elements per lane per tile
 constexpr int kWaveTile = 64 * kSlots;        // 2048 elements per wave tile
-constexpr int kWaveStage = 1024;              // staged output entries per wave (6 bytes each)
 constexpr int kQueue = 256;                   // queued candidates per wave (16 bytes each)
 constexpr int kBlocksPerCU = 3;               // 3 waves per SIMD (VGPR-bound), 40 KB LDS
 // a float4 slot selects up to 4 x 64 elements at once: they must fit an

@@ -56,7 +56,7 @@ constexpr int64_t kGroup = (int64_t)kWaves * kChunk;  // entries per block per r
 // once.
 constexpr int64_t kBlockEntries = 4096;
 constexpr int64_t kMinBlockEntries = 64;
-constexpr int kRemapBlocksPerCU = 128;
+constexpr int kRemapBlocksPerCU = 128;               // grid cap; larger deltas give each block more groups
 constexpr int kRemapFillPerCU = 5;                 // blocks per CU that keep the chip busy
 
 // Whole chunk inside one segment of kNd dimensions: each

@@ -98,3 +98,59 @@ def test_fused_call_with_no_buckets_counts_every_rank(case):
     assert int(cur.item()) == res.idx.size
     assert rank_count.cpu().tolist() == [w[0].size for w in want]
     plan.close()
+
+
+def test_entries_outside_the_plan_or_shard_are_ignored(case):
+    """remap skips offsets outside [0, total) (include/dte.h); apply skips
+    bucket offsets outside a shard."""
+    wl, res, d = case
+    say("case: out-of-range entries")
+    spec = layouts.build_spec(wl)
+    plan = Plan(spec)
+    total = spec.total
+    rng = np.random.default_rng(26080455 + 91)
+    bad = np.array([-1, -(1 << 40), total, total + 1, 1 << 50, -total], np.int64)
+    idx = np.concatenate([res.idx, bad])
+    val = np.concatenate([res.val, np.full(bad.size, 0xBEEF, np.uint16)])
+    perm = rng.permutation(idx.size)
+    idx, val = idx[perm], val[perm]
+    want = oremap.remap(oplan.build_plan(wl), res.idx, res.val)
+    s = torch.cuda.current_stream().cuda_stream
+    m = idx.size
+    d_idx = torch.from_numpy(idx).cuda()
+    d_val = torch.from_numpy(val.view(np.int16)).cuda()
+    count = torch.tensor([m], dtype=torch.int64, device="cuda")
+    off = [torch.empty(m, dtype=torch.int64, device="cuda") for _ in range(spec.nranks)]
+    rv = [torch.empty(m, dtype=torch.int16, device="cuda") for _ in range(spec.nranks)]
+    rank_count = torch.zeros(spec.nranks, dtype=torch.int64, device="cuda")
+    B.dte_remap(plan.handle, d_idx.data_ptr(), d_val.data_ptr(), count.data_ptr(), m,
+                [t.data_ptr() for t in off], [t.data_ptr() for t in rv], [m] * spec.nranks,
+                rank_count.data_ptr(), s)
+    torch.cuda.synchronize()
+    counts = rank_count.cpu().tolist()
+    for r in range(spec.nranks):
+        assert counts[r] == want[r][0].size, r
+        got = off[r][:counts[r]].cpu().numpy()
+        order = got.argsort(kind="stable")
+        assert np.array_equal(got[order], want[r][0]), r
+        assert np.array_equal(rv[r][:counts[r]].cpu().numpy().view(np.uint16)[order],
+                              want[r][1]), r
+    # apply: buckets with offsets outside the shard
+    numel = spec.rank_numel
+    b_off = [np.array([0, -1, numel[r] - 1, numel[r], -(1 << 40), 1 << 45, 5], np.int64)
+             for r in range(spec.nranks)]
+    b_val = [np.arange(7, dtype=np.uint16) + 100 * (r + 1) for r in range(spec.nranks)]
+    shards = [torch.full((n,), 0x33, dtype=torch.int16, device="cuda") for n in numel]
+    dt_off = [torch.from_numpy(x).cuda() for x in b_off]
+    dt_val = [torch.from_numpy(x.view(np.int16)).cuda() for x in b_val]
+    cnt = torch.tensor([7] * spec.nranks, dtype=torch.int64, device="cuda")
+    B.dte_apply(plan.handle, [t.data_ptr() for t in shards], [t.data_ptr() for t in dt_off],
+                [t.data_ptr() for t in dt_val], cnt.data_ptr(), [7] * spec.nranks, s)
+    torch.cuda.synchronize()
+    for r in range(spec.nranks):
+        expect = np.full(numel[r], 0x33, np.uint16)
+        for o, v in zip(b_off[r], b_val[r]):
+            if 0 <= o < numel[r]:
+                expect[o] = v
+        assert np.array_equal(shards[r].cpu().numpy().view(np.uint16), expect), r
+    plan.close()

@@ -74,18 +74,31 @@ def state(wl, k: int, lo: int, hi: int, sc: core.Scalars, threads: int = 1):
     return p_prev, p, m, v
 
 
-def run_window(wl, w: Window, sc: core.Scalars, keep=(), threads: int = 1) -> WindowResult:
-    begin = wl.flat_begins()[w.tensor]
-    p_prev, p, m, v = state(wl, w.tensor, w.lo, w.hi, sc, threads)
-    idx, val, ph = core.detect(p, m, v, sc, begin + w.lo)
+def count_diagnostics(p_prev, ph, p, changed: int) -> Diagnostics:
+    """Reconstruction diagnostics of one window.  The inverse gives a
+    numerical reconstruction of the previous weights, not a bitwise
+    recovery (sec. 4.1), so beside the delta size the oracle counts, per
+    element of the window: binary32 patterns of theta_hat that differ from
+    the true pre-step weights p_prev; BF16 patterns that differ, b(theta_hat)
+    != b(p_prev); the true BF16 changes b(p_prev) != b(p); and the elements
+    that a receiver holding b(p_prev) would keep stale after apply,
+    b(p_prev) != b(theta_hat) == b(p)."""
     b_prev = core.bf16(p_prev)
     b_ph = core.bf16(ph)
     b_p = core.bf16(p)
-    d = Diagnostics(n=w.hi - w.lo, changed=int(idx.size))
+    d = Diagnostics(n=int(p.size), changed=changed)
     d.fp32_recon_mismatch = int(np.count_nonzero(ph.view(np.uint32) != p_prev.view(np.uint32)))
     d.bf16_recon_mismatch = int(np.count_nonzero(b_ph != b_prev))
     d.true_changed = int(np.count_nonzero(b_prev != b_p))
     d.apply_vs_prev_diff = int(np.count_nonzero((b_prev != b_ph) & (b_ph == b_p)))
+    return d
+
+
+def run_window(wl, w: Window, sc: core.Scalars, keep=(), threads: int = 1) -> WindowResult:
+    begin = wl.flat_begins()[w.tensor]
+    p_prev, p, m, v = state(wl, w.tensor, w.lo, w.hi, sc, threads)
+    idx, val, ph = core.detect(p, m, v, sc, begin + w.lo)
+    d = count_diagnostics(p_prev, ph, p, int(idx.size))
     r = WindowResult(w, idx, val, d)
     for name in keep:
         setattr(r, name, locals()[name])

@@ -54,7 +54,7 @@ typedef int32_t dte_status;
 #define DTE_ORDER_FOLDED 0   /* bias corrections folded into two scalars */
 #define DTE_ORDER_LITERAL 1  /* eq. adamw_inverse as printed: four divisions */
 
-/* Hyperparameters of one AdamW step of one parameter group (paper sec. 3.1,
+/* Hyperparameters of one AdamW step of one parameter group (paper sec. 4.1,
  * eq. adamw_moments and eq. adamw_inverse; appendix A): learning rate eta_t,
  * moment coefficients beta1, beta2, epsilon, the group's decoupled weight
  * decay lambda, and the step index t of the step just taken (t >= 1);
@@ -78,7 +78,7 @@ typedef struct {
  *   lrb1  = lr / (1 - beta1^t)      rbc2  = 1 / (1 - beta2^t)
  *   eps   = eps                     decay = 1 - lr * weight_decay
  *   lr    = lr                      bc1 = 1 - beta1^t,  bc2 = 1 - beta2^t
- * With them the inverse of sec. 3.1, eq. adamw_inverse, is evaluated per
+ * With them the inverse of sec. 4.1, eq. adamw_inverse, is evaluated per
  * element, left to right, as
  *   folded:  u = (lrb1 * m) / (sqrt(v * rbc2) + eps)
  *   literal: u = lr * ((m / bc1) / (sqrt(v / bc2) + eps))
@@ -102,11 +102,11 @@ typedef struct {
 dte_status dte_derive_scalars(const dte_adamw_step* hp, dte_scalars* out);
 
 /* Extract the BF16-visible delta of one contiguous range of the flat
- * trainer shard (paper sec. 3.1 reconstruction; sec. 3.2.1 eq.
+ * trainer shard (paper sec. 4.1 reconstruction; sec. 4.2.1 eq.
  * canonical_delta_detection).
  *
  * For each element i in [0, n):
- *   theta_hat = inverse(p[i], m[i], v[i])            (sec. 3.1, see dte_scalars;
+ *   theta_hat = inverse(p[i], m[i], v[i])            (sec. 4.1, see dte_scalars;
  *                                                     in hp->order)
  *   b_old = BF16(theta_hat), b_new = BF16(p[i])     (round to nearest even on
  *           the binary32 pattern; overflow to +-inf; any NaN -> 0x7FC0)
@@ -116,7 +116,7 @@ dte_status dte_derive_scalars(const dte_adamw_step* hp, dte_scalars* out);
  *   out_val = b_new            (target BF16 pattern, not a difference)
  *
  * p, m, v : device, n binary32 each: theta_t, m_t, v_t of the range,
- *           element-aligned (paper sec. 3.1: optimizer-native slices).
+ *           element-aligned (paper sec. 4.1: optimizer-native slices).
  *           16-byte alignment of p, m, v (equal modulo 16) enables vector loads.
  * index_base : flat trainer offset of p[0]; >= 0.
  * hp      : host; the step's hyperparameters (one parameter group per call;
@@ -144,7 +144,7 @@ dte_status dte_extract_delta(const float* p, const float* m, const float* v, int
 int64_t dte_ordered_workspace_bytes(int64_t capacity);
 
 /* dte_extract_delta with the entries in ascending offset order (paper
- * sec. 3.2.2 asks for an ordered sparse payload per sender-receiver pair):
+ * sec. 4.2.2 asks for an ordered sparse payload per sender-receiver pair):
  * the same set of entries, written to out_idx / out_val at positions
  * *cursor, *cursor + 1, ... sorted by offset, and the same cursor
  * semantics.  The order does not depend on timing: repeated calls on the
@@ -163,7 +163,7 @@ dte_status dte_extract_delta_ordered(const float* p, const float* m, const float
                                      int64_t* cursor, void* workspace, int64_t workspace_bytes,
                                      float* out_prev, void* stream);
 
-/* One canonical parameter of the flat trainer shard (paper sec. 3.2.2:
+/* One canonical parameter of the flat trainer shard (paper sec. 4.2.2:
  * sender-local converted tensor of shape n_s): flat_begin is its offset in
  * the shard, shape[0..ndim) its row-major extents (ndim in 1..4). */
 typedef struct {
@@ -173,7 +173,7 @@ typedef struct {
     int64_t shape[DTE_MAX_DIMS];
 } dte_segment;
 
-/* One operation o of the transfer plan T (paper sec. 3.2.2): the
+/* One operation o of the transfer plan T (paper sec. 4.2.2): the
  * hyperrectangular overlap between segment `segment` (shape n_s) and a
  * receiver-local view of shape dst_shape (n_r) that starts at flat offset
  * dst_base of receiver rank `rank`'s buffer.  Source origin a_s, extent e,
@@ -195,7 +195,7 @@ typedef struct {
  * shared by concurrent calls on any streams of the device it was created on. */
 typedef struct dte_plan dte_plan;
 
-/* Validate and upload a transfer plan (paper sec. 3.2.2; Observation 3:
+/* Validate and upload a transfer plan (paper sec. 4.2.2; Observation 3:
  * layouts and therefore T are fixed before synchronisation).
  *
  * segs : host, nseg segments sorted by flat_begin, contiguous from 0 (they
@@ -233,7 +233,7 @@ void dte_plan_destroy(dte_plan* plan);
 dte_status dte_plan_info(const dte_plan* plan, int64_t* total, int32_t* nranks,
                          int32_t* max_replication);
 
-/* Remap a delta into per-receiver buckets (paper sec. 3.2.2: unravel
+/* Remap a delta into per-receiver buckets (paper sec. 4.2.2: unravel
  * eq. canonical_unravel, containment, ravel eq. receiver_local_remapping;
  * partition or replication per the plan).
  *
@@ -246,7 +246,7 @@ dte_status dte_plan_info(const dte_plan* plan, int64_t* total, int32_t* nranks,
  *              entries: receiver-local flat offset and value.
  * rank_count : device int64[nranks], written: entries routed to each rank
  *              (the per-receiver sizes that the paper's first transfer round
- *              sends, zeros included, sec. 3.3).  rank_count[r] >
+ *              sends, zeros included, sec. 4.3).  rank_count[r] >
  *              rank_capacity[r] after synchronisation means bucket r is
  *              incomplete.  Offsets within a bucket are unique; order
  *              unspecified.  Entries whose idx lies outside the plan are
@@ -257,7 +257,7 @@ dte_status dte_remap(const dte_plan* plan, const int64_t* idx, const uint16_t* v
                      uint16_t* const* out_val, const int64_t* rank_capacity,
                      int64_t* rank_count, void* stream);
 
-/* dte_extract_delta and dte_remap in one pass (paper sec. 3.2.1: changed
+/* dte_extract_delta and dte_remap in one pass (paper sec. 4.2.1: changed
  * indices are remapped as soon as they are detected): the changed entries
  * of [index_base, index_base + n) are routed through `plan` straight into
  * the receiver buckets, without the (I, V) arrays.  Arguments as in those
@@ -273,7 +273,7 @@ dte_status dte_extract_remap(const float* p, const float* m, const float* v, int
                              const int64_t* rank_capacity, int64_t* rank_count, int64_t* count,
                              void* stream);
 
-/* Direct sparse apply (paper sec. 3.3, eq. direct_sparse_apply):
+/* Direct sparse apply (paper sec. 4.3, eq. direct_sparse_apply):
  * shards[r][off[r][k]] = val[r][k] for k < min(rank_count[r],
  * rank_capacity[r]), every rank r.  Because values are targets, applying a
  * delta twice equals applying it once.
@@ -285,7 +285,7 @@ dte_status dte_apply(const dte_plan* plan, uint16_t* const* shards, const int64_
                      const uint16_t* const* val, const int64_t* rank_count,
                      const int64_t* rank_capacity, void* stream);
 
-/* The trainer-side step that dte_extract_delta inverts (paper sec. 3.1,
+/* The trainer-side step that dte_extract_delta inverts (paper sec. 4.1,
  * eq. adamw_moments; appendix A, eq. appendix_adamw_forward), in place on
  * device buffers p, m, v (theta, m, v of step t-1 in, of step t out) with
  * gradient g, n elements each, in the same binary32 operation order:

@@ -1,10 +1,10 @@
 /*
  * dte_store.h -- storage-mediated publication of sparse BF16 deltas
- * (AReaL-DTE, paper sec. 3.4, cross-cluster transfer).
+ * (AReaL-DTE, paper sec. 4.4, cross-cluster transfer).
  *
  * Across clusters there is no communication group between trainer and
  * rollout workers, so a version's canonical sparse changes (the (I, V) of
- * sec. 3.2.1, one entry per changed canonical element) travel through a
+ * sec. 4.2.1, one entry per changed canonical element) travel through a
  * shared filesystem: writer ranks serialise only the changed index-value
  * pairs of the partitions they own into compressed chunks, staged through
  * a bounded pinned-memory pipeline; a coordinator commits a version
@@ -59,7 +59,7 @@ typedef struct {
 
 /* A contiguous range [sender_begin, sender_end) of the writer's flat shard
  * that holds whole rows of a box of canonical segment `segment` (the
- * converter's map for a trainer layout such as Megatron-Core, sec. 3.2.1
+ * converter's map for a trainer layout such as Megatron-Core, sec. 4.2.1
  * and appendix B): shard element sender_begin + q, with q = row *
  * local_cols + col, is element (canon_row0 + row, canon_col0 + col) of the
  * segment viewed as rows of canon_cols, i.e. its canonical local index is

@@ -6,14 +6,14 @@ package; the product path (paper_2608_00455_amd) never does, and the two
 share no code.  Inputs come from the seeded generator in `synth`.
 
 Modules, each following the paper's passage named in its header:
-  core   -- step scalars, forward AdamW step, AdamW inversion (sec. 3.1,
-            appendix A), BF16 quantisation and detection (sec. 3.2.1); the
+  core   -- step scalars, forward AdamW step, AdamW inversion (sec. 4.1,
+            appendix A), BF16 quantisation and detection (sec. 4.2.1); the
             binary32 arithmetic is plain C in dte_oracle.c
-  plan   -- transfer plan T (sec. 3.2.2) for the receiver layouts
-  remap  -- unravel / containment / ravel (sec. 3.2.2) and direct sparse
-            apply (sec. 3.3, eq. direct_sparse_apply)
+  plan   -- transfer plan T (sec. 4.2.2) for the receiver layouts
+  remap  -- unravel / containment / ravel (sec. 4.2.2) and direct sparse
+            apply (sec. 4.3, eq. direct_sparse_apply)
   run    -- whole-workload driver (seeded state, forward step, detection;
-            per-group step scalars, sec. 3.1)
+            per-group step scalars, sec. 4.1)
   mcore  -- Megatron-Core sender layout and converter (appendix B,
             eq. mcore_fused_qkv, eq. mcore_tp_shard, eq. qkv_converter):
             detection in the paper's order for one trainer TP rank

@@ -54,7 +54,7 @@ def lib():
 
 
 def derive_scalars(hp) -> Scalars:
-    """Step scalars of the inverse and the forward step (sec. 3.1; appendix A),
+    """Step scalars of the inverse and the forward step (sec. 4.1; appendix A),
     for the operation order hp.order (0 folded, 1 literal eq. adamw_inverse)."""
     s = Scalars()
     rc = lib().oracle_derive_scalars(hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay,
@@ -70,7 +70,7 @@ def _f32(a):
 
 
 def adamw_forward(p_prev, m_prev, v_prev, g, sc: Scalars):
-    """One AdamW step (sec. 3.1, eq. adamw_moments; appendix A forward)."""
+    """One AdamW step (sec. 4.1, eq. adamw_moments; appendix A forward)."""
     p_prev, m_prev, v_prev, g = map(_f32, (p_prev, m_prev, v_prev, g))
     n = p_prev.size
     assert m_prev.size == n and v_prev.size == n and g.size == n
@@ -82,7 +82,7 @@ def adamw_forward(p_prev, m_prev, v_prev, g, sc: Scalars):
 
 
 def invert(p, m, v, sc: Scalars):
-    """theta_hat_{t-1} (sec. 3.1, eq. adamw_inverse)."""
+    """theta_hat_{t-1} (sec. 4.1, eq. adamw_inverse)."""
     p, m, v = map(_f32, (p, m, v))
     n = p.size
     ph = np.empty(n, np.float32)
@@ -92,7 +92,7 @@ def invert(p, m, v, sc: Scalars):
 
 
 def bf16(x):
-    """Q_BF16 then B_16 (sec. 3.2.1): BF16 bit patterns as uint16."""
+    """Q_BF16 then B_16 (sec. 4.2.1): BF16 bit patterns as uint16."""
     x = _f32(x)
     out = np.empty(x.size, np.uint16)
     lib().oracle_bf16_array(x.ctypes.data, x.size, out.ctypes.data)
@@ -106,14 +106,14 @@ def bf16_patterns(first: int, n: int):
 
 
 def detect(p, m, v, sc: Scalars, flat_begin: int = 0):
-    """Converter-aligned detection of one tensor (sec. 3.2.1,
-    eq. canonical_delta_detection), after the inversion of sec. 3.1.
+    """Converter-aligned detection of one tensor (sec. 4.2.1,
+    eq. canonical_delta_detection), after the inversion of sec. 4.1.
 
     Returns (I, V, ph): I = flat trainer offsets (flat_begin + canonical
     index) of the changed elements in ascending order, V = their target BF16
     patterns, ph = the reconstructed previous weights.
     """
-    ph = invert(p, m, v, sc)                 # sec. 3.1
+    ph = invert(p, m, v, sc)                 # sec. 4.1
     b_old = bf16(ph)                         # Q_BF16 of the previous version
     b_new = bf16(p)                          # Q_BF16 of the current version
     mask = b_new != b_old                    # M = B16(new) != B16(old)

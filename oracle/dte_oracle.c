@@ -10,7 +10,7 @@
  * square root).  Shares no code with the HIP path.
  *
  * Operation order (the reading of the paper fixed for both sides): the step
- * scalars of the paper's AdamW inverse (sec. 3.1, eq. adamw_inverse) are
+ * scalars of the paper's AdamW inverse (sec. 4.1, eq. adamw_inverse) are
  * folded once, in binary64, into
  *     LRB1  = lr / (1 - beta1^t)        (step size with bias correction 1)
  *     RBC2  = 1 / (1 - beta2^t)         (reciprocal of bias correction 2)
@@ -19,7 +19,7 @@
  * each rounded once to binary32.  Then per element
  *     u  = (LRB1 * m) / (sqrt(v * RBC2) + EPS)
  *     forward (appendix A, eq. appendix_adamw_forward):   p  = DECAY * p_prev - u
- *     inverse (sec. 3.1, eq. adamw_inverse):              ph = (p + u) / DECAY
+ *     inverse (sec. 4.1, eq. adamw_inverse):              ph = (p + u) / DECAY
  * which is the paper's expression with the bias corrections folded into
  * the two scalars, evaluated left to right.
  *
@@ -40,7 +40,7 @@ typedef struct {
     int32_t order;                  /* 0: folded, 1: literal */
 } oracle_scalars;
 
-/* Step scalars (sec. 3.1, eq. adamw_inverse; appendix A): binary64 math,
+/* Step scalars (sec. 4.1, eq. adamw_inverse; appendix A): binary64 math,
  * one rounding to binary32 each.  Returns 0, or -1 on invalid input. */
 int oracle_derive_scalars(double lr, double beta1, double beta2, double eps, double wd,
                           int64_t step, int32_t order, oracle_scalars* out)
@@ -86,7 +86,7 @@ static float oracle_step_term(float m, float v, const oracle_scalars* s)
     return num / den;
 }
 
-/* One forward AdamW step (sec. 3.1, eq. adamw_moments; appendix A,
+/* One forward AdamW step (sec. 4.1, eq. adamw_moments; appendix A,
  * eq. appendix_adamw_forward), producing the post-step state the method
  * reads.  Element-wise over n elements. */
 void oracle_adamw_forward(const float* p_prev, const float* m_prev, const float* v_prev,
@@ -110,7 +110,7 @@ void oracle_adamw_forward(const float* p_prev, const float* m_prev, const float*
     }
 }
 
-/* AdamW inversion (sec. 3.1, eq. adamw_inverse): theta_hat_{t-1} per
+/* AdamW inversion (sec. 4.1, eq. adamw_inverse): theta_hat_{t-1} per
  * element from theta_t, m_t, v_t. */
 void oracle_invert(const float* p, const float* m, const float* v, int64_t n,
                    const oracle_scalars* s, float* p_hat)
@@ -122,7 +122,7 @@ void oracle_invert(const float* p, const float* m, const float* v, int64_t n,
     }
 }
 
-/* BF16 quantisation Q_BF16 of sec. 3.2.1, as round-to-nearest-even of the
+/* BF16 quantisation Q_BF16 of sec. 4.2.1, as round-to-nearest-even of the
  * binary32 bit pattern: keep the upper 16 bits after adding half an ulp of
  * BF16 (0x7FFF) plus the parity of the kept part, so exact ties go to the
  * even pattern; overflow carries into +-inf; subnormals are kept.  Any NaN

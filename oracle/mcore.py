@@ -3,7 +3,7 @@
 The trainer holds optimizer-native MCore tensors (appendix B): the fused
 GQA projection W_QKV^MCore built per eq. mcore_fused_qkv, stored per
 tensor-parallel rank as the row range R_r of eq. mcore_tp_shard.  The
-paper's converter C (sec. 3.2.1, eq. aligned_conversion) gathers the TP
+paper's converter C (sec. 4.2.1, eq. aligned_conversion) gathers the TP
 pieces of one converter unit and unpacks them into the canonical tensors
 (eq. canonical_qkv_unpacking, eq. qkv_converter); detection then compares
 BF16 patterns in that canonical space (eq. canonical_delta_detection).
@@ -20,8 +20,8 @@ principle covers the other fused or sharded parameters):
   linear_fc1, linear_fc2], final layernorm, output layer.
   Each trainer rank detects and sends the canonical elements it holds.
 
-The arithmetic is that of core (inversion in MCore space, sec. 3.1; BF16
-detection after conversion, sec. 3.2.1); this module only moves elements.
+The arithmetic is that of core (inversion in MCore space, sec. 4.1; BF16
+detection after conversion, sec. 4.2.1); this module only moves elements.
 """
 from __future__ import annotations
 
@@ -157,7 +157,7 @@ def extract(wl, hp=None, threads: int = 0) -> Result:
     unit at a time: the unit's MCore tensors on every TP rank (the seeded
     canonical state packed per eq. mcore_fused_qkv and sharded per
     eq. mcore_tp_shard), the inversion on each rank's optimizer-native
-    shard (sec. 3.1), gather and conversion of both versions
+    shard (sec. 4.1), gather and conversion of both versions
     (eq. aligned_conversion), BF16 comparison per canonical tensor
     (eq. canonical_delta_detection); kept are the changes to elements that
     the sender rank holds."""

@@ -1,6 +1,6 @@
 """Oracle's transfer plan (test infrastructure only).
 
-Builds the paper's transfer plan T (sec. 3.2.2): for each canonical
+Builds the paper's transfer plan T (sec. 4.2.2): for each canonical
 parameter p and receiver r, the hyperrectangular overlap between the
 sender's canonical tensor view (shape n_s) and the receiver-local shard
 (shape n_r), given by the origins a_s, a_r and the extent e.

@@ -1,7 +1,7 @@
 """Oracle's receiver-space remap and direct sparse apply (test
 infrastructure only).
 
-remap: sec. 3.2.2 -- for each changed flat index, u = unravel(i, n_s)
+remap: sec. 4.2.2 -- for each changed flat index, u = unravel(i, n_s)
 (eq. canonical_unravel); the change belongs to op o when
 a_s <= u < a_s + e component-wise; its receiver index is
 j_r = ravel(u - a_s + a_r, n_r) (eq. receiver_local_remapping), here offset
@@ -9,7 +9,7 @@ by the flat base of the receiver view inside rank r's buffer.  Every op of
 the plan is applied, so a change is partitioned or replicated as the layout
 says.  The value is carried unchanged.
 
-apply: sec. 3.3, eq. direct_sparse_apply -- vec(W_r)[I] <- V.
+apply: sec. 4.3, eq. direct_sparse_apply -- vec(W_r)[I] <- V.
 """
 from __future__ import annotations
 

@@ -1,10 +1,10 @@
 """Oracle driver: a whole workload on the CPU (test infrastructure only).
 
 State generation (seeded draws, then one forward AdamW step), then the
-method in the paper's order: inversion (sec. 3.1), BF16 detection
-(sec. 3.2.1), receiver remap (sec. 3.2.2), direct apply (sec. 3.3).
+method in the paper's order: inversion (sec. 4.1), BF16 detection
+(sec. 4.2.1), receiver remap (sec. 4.2.2), direct apply (sec. 4.3).
 Tensors are processed one at a time (the paper's streaming per converter
-unit, sec. 3.1) and, for large tensors, in element windows; a thread pool
+unit, sec. 4.1) and, for large tensors, in element windows; a thread pool
 runs independent windows side by side.
 """
 from __future__ import annotations
@@ -117,7 +117,7 @@ def windows(wl, max_window: int = 1 << 24, tensors=None) -> List[Window]:
 
 def scalars(wl, hp=None) -> List[core.Scalars]:
     """Step scalars of every tensor, from its parameter group's
-    hyperparameters (the weight-decay coefficient is per group, sec. 3.1)."""
+    hyperparameters (the weight-decay coefficient is per group, sec. 4.1)."""
     return [core.derive_scalars(wl.group_hp(k, hp)) for k in range(len(wl.tensors))]
 
 

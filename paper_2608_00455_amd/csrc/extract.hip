@@ -1,5 +1,5 @@
-// Delta extraction for gfx950: AdamW inversion (paper sec. 3.1,
-// eq. adamw_inverse), BF16 quantisation and bit comparison (sec. 3.2.1,
+// Delta extraction for gfx950: AdamW inversion (paper sec. 4.1,
+// eq. adamw_inverse), BF16 quantisation and bit comparison (sec. 4.2.1,
 // eq. canonical_delta_detection) and stream compaction of the changed
 // elements, fused in one streaming pass over theta, m, v.
 //
@@ -158,7 +158,7 @@ __device__ __forceinline__ bool proven_unchanged(float p, float m, float v, cons
            (hi == hi);
 }
 
-// Exact inverse and change test of one element (sec. 3.1 / 3.2.1).
+// Exact inverse and change test of one element (sec. 4.1 / 4.2.1).
 template <bool kDecayOne, bool kLit>
 __device__ __forceinline__ float exact_prev(float p, float m, float v, const ExtractParams& a)
 {

@@ -1,4 +1,4 @@
-// Receiver-space remap (paper sec. 3.2.2) and direct sparse apply (sec. 3.3,
+// Receiver-space remap (paper sec. 4.2.2) and direct sparse apply (sec. 4.3,
 // eq. direct_sparse_apply) for gfx950.
 //
 // Remap: every entry (flat trainer offset i, BF16 value) finds its segment

@@ -1,5 +1,5 @@
 // Device-side routing of delta entries through a transfer plan (paper
-// sec. 3.2.2): segment lookup, unravel (eq. canonical_unravel), containment
+// sec. 4.2.2): segment lookup, unravel (eq. canonical_unravel), containment
 // and ravel (eq. receiver_local_remapping).  Shared by the remap kernel and
 // the extract kernel's routing flush; not part of the C ABI.
 #pragma once

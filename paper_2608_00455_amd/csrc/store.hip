@@ -1,4 +1,4 @@
-// Storage-mediated publication of sparse BF16 deltas (paper sec. 3.4,
+// Storage-mediated publication of sparse BF16 deltas (paper sec. 4.4,
 // cross-cluster transfer): chunk serialisation, Zstandard compression,
 // XXH64 checksums, writer parts, the committed manifest and the version
 // chain on the host; narrowing of flat offsets to segment-local 32-bit

@@ -1,4 +1,4 @@
-"""Transfer-plan construction for the receiver layouts (paper sec. 3.2.2:
+"""Transfer-plan construction for the receiver layouts (paper sec. 4.2.2:
 the plan T is precomputed from sender and receiver shard metadata;
 Observation 3: the layouts fix it before synchronisation).
 
@@ -9,7 +9,7 @@ Sender side: the flat trainer shard is a sequence of segments (one
 dte_segment each).  With the canonical layout they are the Hugging Face
 tensors in parameter order.  With the Megatron-Core layout they are one
 trainer tensor-parallel rank's optimizer-native tensors, and the converter
-of sec. 3.2.1 (appendix B) is folded into the plan: each segment is a set of
+of sec. 4.2.1 (appendix B) is folded into the plan: each segment is a set of
 pieces, each piece a box of the segment that is a box of one canonical
 tensor (fused linear_qkv: per key/value group j the g query heads, then K_j,
 then V_j, eq. mcore_fused_qkv, rank r holding rows R_r, eq. mcore_tp_shard;

@@ -136,7 +136,7 @@ class DeltaPipeline:
 
     def extract_runs(self, p, m, v, runs, out_prev=None, stream=None):
         """One dte_extract_delta per run (begin, end, hp) of the flat shard,
-        appending to the same delta (parameter groups, sec. 3.1)."""
+        appending to the same delta (parameter groups, sec. 4.1)."""
         for b, e, hp in runs:
             self.extract(p[b:e], m[b:e], v[b:e], hp, n=e - b, index_base=b,
                          out_prev=out_prev[b:e] if out_prev is not None else None,

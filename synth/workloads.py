@@ -7,11 +7,11 @@ method's arithmetic: neither the AdamW step, nor the BF16 rounding, nor the
 transfer-plan construction lives here.
 
 Shapes follow the Qwen3 family in Hugging Face parameter order (the
-canonical space of the paper's converter-aligned detection, sec. 3.2.1;
+canonical space of the paper's converter-aligned detection, sec. 4.2.1;
 canonical Q/K/V shapes are eq. canonical_qkv_shapes of appendix B).
 Value scales: p_prev sigma 0.02, m_prev sigma 1e-4, v_prev = |sigma 1e-6|,
 gradient sigma 1e-3, drawn per element by the seeded generator of
-synth/csrc/philox.h.  The paper's evaluation (sec. 4.1) uses
+synth/csrc/philox.h.  The paper's evaluation (sec. 5.1) uses
 training-generated RL states of Qwen3-8B and Qwen3-30B-A3B; these seeded
 states of the same shapes stand in for them.
 """

@@ -1,8 +1,8 @@
 """One transfer plan shared by concurrent calls on two streams (the plan
 is immutable once created, include/dte.h): two different deltas are
 remapped and applied at the same time, each into its own buckets and
-shards, and each result equals the oracle's remap (sec. 3.2.2) and apply
-(sec. 3.3) of its own delta."""
+shards, and each result equals the oracle's remap (sec. 4.2.2) and apply
+(sec. 4.3) of its own delta."""
 import sys
 
 import numpy as np

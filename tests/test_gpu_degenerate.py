@@ -1,6 +1,6 @@
 """Degenerate calls the C ABI allows: zero capacities with NULL output
 pointers (count-only calls).  The counts must equal the oracle's (sec.
-3.2.1 detection, sec. 3.2.2 remap) and nothing may be written."""
+4.2.1 detection, sec. 4.2.2 remap) and nothing may be written."""
 import sys
 
 import numpy as np

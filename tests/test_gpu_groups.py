@@ -1,5 +1,5 @@
 """GPU parity with two parameter groups (norms without weight decay,
-sec. 3.1): the state is generated and the delta extracted per run of
+sec. 4.1): the state is generated and the delta extracted per run of
 segments with equal step scalars, appending to one delta; compared bit for
 bit with the oracle, including the reconstructed weights."""
 import sys

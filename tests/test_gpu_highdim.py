@@ -3,7 +3,7 @@ have one to four dimensions (the plan format allows four; the model
 workloads only use vectors and matrices).
 
 The plan is written out here twice, as the oracle's Plan and as the C-ABI
-structs; the oracle's remap (sec. 3.2.2) is the reference.  Inputs are
+structs; the oracle's remap (sec. 4.2.2) is the reference.  Inputs are
 seeded synthetic draws; the post-step state comes from the oracle's
 forward step.
 """

@@ -1,4 +1,4 @@
-"""GPU side of the storage-mediated path (paper sec. 3.4): an ordered delta
+"""GPU side of the storage-mediated path (paper sec. 4.4): an ordered delta
 published straight from the device and read back into device memory equals
 the oracle's delta; remapped and applied on the GPU, it gives the receiver
 layout of the new BF16 weights.  An unordered delta is refused."""

@@ -1,4 +1,4 @@
-"""Parameter groups (sec. 3.1: the weight-decay coefficient belongs to the
+"""Parameter groups (sec. 4.1: the weight-decay coefficient belongs to the
 parameter group), on the CPU.
 
 Pin of the oracle's group handling against two ungrouped runs: with the

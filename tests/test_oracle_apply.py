@@ -1,5 +1,5 @@
-"""Pins of the oracle's detection/compaction (sec. 3.2.1) and direct sparse
-apply (sec. 3.3): brute force on small inputs and the invariants of
+"""Pins of the oracle's detection/compaction (sec. 4.2.1) and direct sparse
+apply (sec. 4.3): brute force on small inputs and the invariants of
 sending target values (idempotent apply, untouched elements kept,
 apply(layout(old), delta) == layout(new))."""
 import numpy as np

@@ -1,9 +1,9 @@
-"""Pins of the oracle's binary32 arithmetic (sec. 3.1, appendix A).
+"""Pins of the oracle's binary32 arithmetic (sec. 4.1, appendix A).
 
 Against: exact rational evaluation of the step scalars and of the paper's
 inverse (eq. adamw_inverse), torch.optim.AdamW for the forward step, the
 round-trip invariant inverse(forward(x)) ~ x (exact in exact arithmetic,
-sec. 3.1), and closed-form special cases.  A per-operation binary64
+sec. 4.1), and closed-form special cases.  A per-operation binary64
 evaluation rounded to binary32 (exact for + - * / sqrt by the double-
 rounding theorem, 53 >= 2*24 + 2) checks the C build itself: no fused
 multiply-add, no flushed subnormals, correctly rounded divide and sqrt.
@@ -141,7 +141,7 @@ def test_inverse_within_bound_of_exact(lr):
 
 @pytest.mark.parametrize("lr", [1e-7, 1e-6, 1e-5, 1e-4])
 def test_round_trip_recovers_previous_weights(lr):
-    """Inverse after forward returns p_prev up to rounding (sec. 3.1: exact
+    """Inverse after forward returns p_prev up to rounding (sec. 4.1: exact
     in exact arithmetic): within 2 ulp of the larger of |p_prev| and the
     step |p - p_prev|, and mostly bit-exact."""
     hp = W.StepHP(lr=lr)

@@ -1,4 +1,4 @@
-"""Pins of the oracle's BF16 quantisation and change test (sec. 3.2.1).
+"""Pins of the oracle's BF16 quantisation and change test (sec. 4.2.1).
 
 Against: a hand-derived table (golden fixture), exact rational rounding in
 Python integers, and torch's CPU float->bfloat16 cast over every binary32

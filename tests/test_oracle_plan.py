@@ -1,4 +1,4 @@
-"""Pins of the oracle's transfer plan and remap (sec. 3.2.2).
+"""Pins of the oracle's transfer plan and remap (sec. 4.2.2).
 
 The remap of every canonical flat offset must reproduce the dense receiver
 route (tests/dense_route.py) exactly: this shows the plan's unravel /

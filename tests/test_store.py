@@ -1,4 +1,4 @@
-"""Storage-mediated publication (paper sec. 3.4), host side, no GPU.
+"""Storage-mediated publication (paper sec. 4.4), host side, no GPU.
 
 The stored files are checked by a reader written here from the format's
 description (Python struct, the `xxhash` package for XXH64, libzstd through
@@ -216,7 +216,7 @@ def test_writer_rejects_bad_input(tmp_path, delta):
 
 
 def _mcore_delta_in_sender_offsets(wl):
-    """The oracle's delta of the rank's elements (sec. 3.2.1, in canonical
+    """The oracle's delta of the rank's elements (sec. 4.2.1, in canonical
     offsets) expressed as offsets of the rank's own shard, ascending."""
     from oracle import mcore
     ci = mcore.canonical_index(wl)

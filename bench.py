@@ -54,70 +54,115 @@ def workload(name, lr):
     raise SystemExit("unknown workload %r" % name)
 
 
-def cpu_baseline(seconds_target=10.0):
-    """The oracle (inversion, BF16 detection, nonzero, remap, apply) timed
-    on the host cores over a bounded sample of the default workload: one
-    Qwen3-8B layer (192,946,432 elements, receiver TP=4), its post-step
-    state generated once untimed, then whole oracle passes over it repeated
-    until at least `seconds_target` seconds of oracle work are timed."""
-    from concurrent.futures import ThreadPoolExecutor
+def cpu_baseline(procs=0):
+    """The oracle timed on the host cores: inversion, BF16 detection,
+    nonzero, remap and apply over the tiny block and four Qwen3-8B layers at
+    lr 1e-6 (a bounded sample of the benchmark's workload), their post-step
+    states generated first (untimed); (i) in one process and (ii) with a
+    pool of P processes.  `value` is the pool's rate on the four layers."""
+    from oracle import timing
 
-    import numpy as np
-
-    import synth
-    from oracle import core, plan, remap, run
-    from synth import workloads as W
-
-    threads = synth.default_threads()
-    wl = W.qwen3_8b_layers_sweep(1e-6, layers=1)
-    pl = plan.build_plan(wl)
-    sc = core.derive_scalars(wl.hp)
-    wins = run.windows(wl, 1 << 22)
-    begins = wl.flat_begins()
-    with ThreadPoolExecutor(threads) as ex:
-        states = list(ex.map(lambda w: run.state(wl, w.tensor, w.lo, w.hi, sc), wins))
-    shards = [np.zeros(n, np.uint16) for n in pl.rank_numel]
-
-    def one_pass(ex):
-        parts = list(ex.map(
-            lambda a: core.detect(a[1][1], a[1][2], a[1][3], sc, begins[a[0].tensor] + a[0].lo)[:2],
-            zip(wins, states)))
-        idx = np.concatenate([x[0] for x in parts])
-        val = np.concatenate([x[1] for x in parts])
-        remap.apply(shards, remap.remap(pl, idx, val))
-
-    secs, passes = 0.0, 0
-    with ThreadPoolExecutor(threads) as ex:
-        while secs < seconds_target and passes < 200:
-            t0 = time.perf_counter()
-            one_pass(ex)
-            secs += time.perf_counter() - t0
-            passes += 1
-    return {"value": passes * wl.numel / secs, "unit": "elements/s", "cores": threads,
+    res = timing.baseline(procs)
+    big = res["runs"][-1]
+    return {"value": big["pool_elements_per_s"], "unit": "elements/s", "cores": res["procs"],
             "kind": "oracle",
-            "sample": "%d passes over one Qwen3-8B layer (%d elements, receiver TP=4, "
-                      "lr 1e-6): inversion + BF16 detection + nonzero + remap + apply, "
-                      "%d threads; state generated once, untimed; %s"
-                      % (passes, wl.numel, threads, run.host_description()),
-            "seconds": secs}
+            "sample": "oracle inversion + BF16 detection + nonzero + remap + apply over every "
+                      "element of %s; one process %.2f s, %d processes %.2f s; also %s; "
+                      "states generated beforehand, untimed; %s"
+                      % (big["workload"], big["single_process_s"], res["procs"], big["pool_s"],
+                         ", ".join("%s %.3f / %.3f s" % (r["workload"], r["single_process_s"],
+                                                         r["pool_s"])
+                                   for r in res["runs"][:-1]), res["cpu_model"]),
+            "cpu_model": res["cpu_model"], "procs": res["procs"],
+            "single_process_elements_per_s": big["single_process_elements_per_s"],
+            "runs": res["runs"]}
 
 
 def measured_traffic(workload_name, kernel, mode):
     """HBM bytes per call of the dominant kernel(s) from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE record (scaled by a plain copy's
     counter reading), or None when there is no record for this workload and
-    mode or the kernel source changed since the counters were taken."""
-    import hashlib
+    mode or the built kernels' machine code differs from the code the
+    counters were taken on."""
+    from paper_2608_00455_amd import devcode
     path = os.path.join(ROOT, "profiles", "%s_%s_traffic.json" % (kernel, workload_name))
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     if rec.get("mode") != mode:
         return None
-    src = os.path.join(ROOT, rec["kernel_source"])
-    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["kernel_source_sha256"]:
+    lib = os.path.join(ROOT, rec["library"])
+    if devcode.kernel_sha256(lib, rec["kernel_symbols"]) != rec["device_code_sha256"]:
         return None
     return rec["traffic_bytes_per_launch"]
+
+
+def ceilings(p, m, v, pipe, stream, reps=5):
+    """Second denominators measured on the same GPU and buffers: the rate of
+    a plain read of theta, m, v (12 bytes per element, extract's access
+    pattern, no arithmetic, no stores; best of 2, 3 and 4 blocks per CU) and
+    the time of writing whole 64-byte lines at every apply address of the
+    step's buckets (into scratch buffers of the shards' size; best of 4, 8
+    and 16 blocks per CU)."""
+    import ctypes
+
+    import torch
+
+    from paper_2608_00455_amd import build as dte_build
+
+    lib = ctypes.CDLL(dte_build.CEIL_LIB)
+    P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    lib.ceil_read3_waves.restype = I64
+    lib.ceil_read3_waves.argtypes = [I32]
+    lib.ceil_read3.restype = ctypes.c_int
+    lib.ceil_read3.argtypes = [P, P, P, I64, I32, P, P]
+    lib.ceil_line_writes.restype = ctypes.c_int
+    lib.ceil_line_writes.argtypes = [I32, P, P, P, P, P, I32, P]
+    s = stream.cuda_stream
+
+    def timed(fn, name):
+        best = None
+        for _ in range(reps + 1):                       # the first is a warm-up
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            rc = fn()
+            if rc != 0:
+                raise RuntimeError("%s failed (%d)" % (name, rc))
+            b.record(stream)
+            b.synchronize()
+            ms = a.elapsed_time(b)
+            best = ms if best is None or ms < best else best
+        return best
+
+    n = p.numel() // 2048 * 2048
+    out = {}
+    best = None
+    for bpc in (2, 3, 4):
+        sink = torch.zeros(64 * lib.ceil_read3_waves(bpc), dtype=torch.int32, device="cuda")
+        ms = timed(lambda: lib.ceil_read3(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, bpc,
+                                          sink.data_ptr(), s), "ceil_read3")
+        if best is None or ms < best[0]:
+            best = (ms, bpc)
+        del sink
+    out["read_stream"] = {"gbs": 12 * n / (best[0] / 1e3) / 1e9, "ms": best[0],
+                          "blocks_per_cu": best[1], "bytes": 12 * n}
+    R = len(pipe.shards)
+    if R <= 16:
+        scratch = [torch.empty_like(t) for t in pipe.shards]
+        arr = lambda T, xs: (T * R)(*xs)                # noqa: E731
+        dst = arr(ctypes.c_void_p, [t.data_ptr() for t in scratch])
+        off = arr(ctypes.c_void_p, [t.data_ptr() for t in pipe.off])
+        cap = arr(ctypes.c_int64, pipe.rank_capacity)
+        numel = arr(ctypes.c_int64, [t.numel() for t in pipe.shards])
+        best = None
+        for bpc in (4, 8, 16):
+            ms = timed(lambda: lib.ceil_line_writes(R, dst, off, pipe.rank_count.data_ptr(), cap,
+                                                    numel, bpc, s), "ceil_line_writes")
+            best = ms if best is None or ms < best else best
+        out["apply_scattered_lines"] = {"ms": best}
+        del scratch
+    torch.cuda.empty_cache()
+    return out
 
 
 def storage_leg(root, wl, spec, p, m, v, hp, cap):
@@ -179,6 +224,13 @@ def copy_calibration(gib):
     return 0
 
 
+def _stats(xs):
+    xs = sorted(xs)
+    k = len(xs)
+    med = xs[k // 2] if k % 2 else 0.5 * (xs[k // 2 - 1] + xs[k // 2])
+    return {"mean": sum(xs) / k, "median": med, "min": xs[0], "max": xs[-1]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,9 +251,18 @@ def main():
                     help="delta buffer size as a fraction of the elements (default 0.02, "
                          "0.25 for the learning-rate sweep)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-procs", type=int, default=0,
+                    help="processes of the oracle's pool run (default: the usable cores)")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the reference read-stream and scattered-line measurements")
+    ap.add_argument("--flush-gb", type=float, default=None, metavar="GB",
+                    help="touch this many GB (read and write) before every timed step, "
+                         "outside the step's own events (default: 1 GB when theta, m, v "
+                         "occupy less than 2 GB, so that they cannot stay in the 256 MB "
+                         "last-level cache between steps; else 0)")
     ap.add_argument("--settle", type=float, default=15.0, metavar="SECONDS",
-                    help="wait before allocating the state: device memory that a process "
+                    help="wait before allocating the state (less the time of the CPU "
+                         "baseline, which runs first): device memory that a process "
                          "released moments earlier is handed out in less contiguous pieces "
                          "until the driver has reclaimed it, which slows streaming kernels")
     ap.add_argument("--store", default=None, metavar="DIR",
@@ -216,6 +277,16 @@ def main():
         print("bench.py measures one GPU; the multi-GPU exchange is not implemented "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         return 2
+
+    cpu, cpu_s = None, 0.0
+    if not args.no_cpu_baseline and args.copy_calibration <= 0:
+        # before any GPU work: the oracle's worker processes are forked from a
+        # process that has not initialised the GPU
+        log("bench: timing the CPU oracle")
+        t = time.perf_counter()
+        cpu = cpu_baseline(args.cpu_procs)
+        cpu_s = time.perf_counter() - t
+        log("bench: CPU oracle done in %.1f s" % cpu_s)
 
     import torch
 
@@ -233,9 +304,10 @@ def main():
     if args.literal:
         hp = type(hp)(lr=hp.lr, beta1=hp.beta1, beta2=hp.beta2, eps=hp.eps,
                       weight_decay=hp.weight_decay, step=hp.step, order=W.ORDER_LITERAL)
-    if args.settle > 0:
-        log("bench: settling %.0f s before allocating" % args.settle)
-        time.sleep(args.settle)
+    settle = max(0.0, args.settle - cpu_s)
+    if settle > 0:
+        log("bench: settling %.0f s before allocating" % settle)
+        time.sleep(settle)
     spec = layouts.build_spec(wl)
     n = spec.total                           # elements of the trainer shard
     log("bench: workload %s, %d elements, lr %g" % (wl.name, n, hp.lr))
@@ -251,62 +323,69 @@ def main():
     runs = group_runs(wl, hp)
     stream = torch.cuda.current_stream()
     apply_only = args.workload.endswith("_apply")
+    flush_gb = args.flush_gb if args.flush_gb is not None else (1.0 if 12 * n < 2e9 else 0.0)
+    flush = (torch.zeros(int(flush_gb * 1e9) // 8, dtype=torch.float32, device="cuda")
+             if flush_gb > 0 else None)
 
+    # events per step: 0 step start (before the cursor reset), 1 extract
+    # start, 2 extract end, 3 remap end, 4 apply end
     def step(ev=None):
+        rec = (lambda i: ev[i].record(stream)) if ev else (lambda i: None)
+        rec(0)
         if apply_only:
-            if ev:
-                ev[0].record(stream)
+            rec(1)
+            rec(2)
+            rec(3)
             pipe.apply()
-            if ev:
-                ev[1].record(stream)
+            rec(4)
             return
         if args.fused:
             pipe.cursor.zero_()
             pipe.rank_count.zero_()
-            if ev:
-                ev[0].record(stream)
+            rec(1)
             for b, e, h in runs:
                 if len(runs) == 1:
                     pipe.extract_remap(p, m, v, h)
                 else:
                     pipe.extract_remap(p[b:e], m[b:e], v[b:e], h, n=e - b, index_base=b)
-            if ev:
-                ev[1].record(stream)
-                ev[2].record(stream)
+            rec(2)
+            rec(3)
         else:
             pipe.reset()
-            if ev:
-                ev[0].record(stream)
+            rec(1)
             if len(runs) == 1:
                 pipe.extract(p, m, v, hp)
             else:
                 pipe.extract_runs(p, m, v, runs)
-            if ev:
-                ev[1].record(stream)
+            rec(2)
             pipe.remap()
-            if ev:
-                ev[2].record(stream)
+            rec(3)
         pipe.apply()
-        if ev:
-            ev[3].record(stream)
+        rec(4)
 
     if apply_only:                           # delta and buckets prepared untimed
         pipe.step(p, m, v, hp)
     for _ in range(args.warmup):
+        if flush is not None:
+            flush.add_(1.0)
         step()
     torch.cuda.synchronize()
-    nev = 2 if apply_only else 4
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     for k in range(args.steps):
+        if flush is not None:
+            flush.add_(1.0)                  # reads and writes flush_gb GB, outside the step
         step(evs[k])
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
-    ms_step = total_ms / args.steps
+    per_step = [e[0].elapsed_time(e[4]) for e in evs]
+    # with a cache flush between steps the step time is the steps' own
+    # events; else the whole bracketed interval
+    ms_step = sum(per_step) / args.steps if flush is not None else total_ms / args.steps
     changed = int(pipe.cursor.item())
     counts = pipe.rank_count.cpu().tolist()
     routed = int(sum(counts))
@@ -314,18 +393,18 @@ def main():
         log("bench: capacity exceeded (changed %d, capacity %d)" % (changed, cap))
         return 3
     c = changed / n
+    ext = _stats([e[1].elapsed_time(e[2]) for e in evs])
+    rem = _stats([e[2].elapsed_time(e[3]) for e in evs])
+    app = _stats([e[3].elapsed_time(e[4]) for e in evs])
 
     if apply_only:
-        k_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+        k = app
         k_bytes = routed * (8 + 2 + 2)       # read offset + value, write value
         value = routed / (ms_step / 1e3)
         metric_unit = "entries/s"
         kernel = "apply"
     else:
-        ext_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
-        rem_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
-        app_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
-        k_ms = ext_ms
+        k = ext
         if args.fused:                        # read theta, m, v; write (offset, value) per route
             k_bytes = 12 * n + 10 * routed
         else:                                 # read theta, m, v; write (idx, val)
@@ -339,7 +418,7 @@ def main():
         step_bytes = 12 * n + 10 * routed + 12 * routed
     else:
         step_bytes = 12 * n + 10 * changed + 10 * changed + 10 * routed + 12 * routed
-    achieved = k_bytes / (k_ms / 1e3) / 1e9
+    achieved = k_bytes / (k["mean"] / 1e3) / 1e9
     # the counters were taken for the default configuration only (folded
     # order, unordered output, one parameter group)
     default_mode = not (args.ordered or args.fused or args.literal or args.norm_group)
@@ -357,30 +436,48 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
-        "config": {"workload": wl.name, "elements": n, "changed": changed, "extract_calls": len(runs), "settle_s": args.settle,
-                   "ordered": ordered, "fused": bool(args.fused), "order": "literal" if args.literal else "folded",
+        "config": {"workload": wl.name, "elements": n, "changed": changed,
+                   "extract_calls": len(runs), "settle_s": settle, "ordered": ordered,
+                   "fused": bool(args.fused), "order": "literal" if args.literal else "folded",
                    "change_fraction": c, "receiver_ranks": len(counts),
                    "routed_entries": routed, "lr": hp.lr,
                    "step_algorithmic_bytes": step_bytes,
                    "step_gbs": step_bytes / (ms_step / 1e3) / 1e9,
-                   "step_frac_of_hbm_peak": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS},
+                   "step_frac_of_hbm_peak": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS,
+                   "flush_gb_between_steps": flush_gb},
+        "timing": {"step_ms": _stats(per_step), "bracket_ms_per_step": total_ms / args.steps,
+                   "extract_ms": ext, "remap_ms": rem, "apply_ms": app},
         "roofline": {"kernel": kernel, "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": (measured_traffic(wl.name, kernel, "unordered")
                                  if default_mode else None),
-                     "kernel_ms": k_ms,
+                     "kernel_ms": k["mean"], "kernel_ms_median": k["median"],
                      "bytes_per_launch": k_bytes},
     }
     if not apply_only:
-        out["config"].update({"extract_ms": ext_ms, "remap_ms": rem_ms, "apply_ms": app_ms})
+        out["config"].update({"extract_ms": ext["mean"], "remap_ms": rem["mean"],
+                              "apply_ms": app["mean"]})
+    if flush is not None:
+        del flush
+        torch.cuda.empty_cache()
+    if not args.no_ceilings:
+        log("bench: reference read stream and scattered lines")
+        ce = ceilings(p, m, v, pipe, stream)
+        rs = ce["read_stream"]
+        if kernel == "extract":
+            rs["kernel_frac"] = achieved / rs["gbs"]
+        if "apply_scattered_lines" in ce:
+            ce["apply_scattered_lines"]["apply_ms"] = app["mean"]
+            ce["apply_scattered_lines"]["apply_frac"] = \
+                ce["apply_scattered_lines"]["ms"] / app["mean"]
+        out["roofline"]["ceilings"] = ce
     if args.store and not apply_only:
         out["storage"] = storage_leg(args.store, wl, spec, p, m, v, hp, cap)
     del p, m, v
     pipe.close()
     torch.cuda.empty_cache()
-    if not args.no_cpu_baseline:
-        log("bench: timing the CPU oracle on a sample")
-        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
     return 0
 

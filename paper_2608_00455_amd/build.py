@@ -1,4 +1,6 @@
-"""Build libdte.so (HIP, gfx950) in-tree.
+"""Build libdte.so (HIP, gfx950) in-tree, and libceilings.so (the
+benchmark's reference kernels: a plain read stream and whole-line scattered
+writes, outside the C ABI).
 
 Floating-point flags: no contraction into fused multiply-add, IEEE
 subnormals, correctly rounded binary32 divide and square root, no packed
@@ -13,6 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdte.so")
 SOURCES = ["dte_api.hip", "extract.hip", "remap.hip", "store.hip"]
+CEIL_LIB = os.path.join(HERE, "libceilings.so")
+CEIL_SOURCES = ["ceilings.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -28,9 +32,12 @@ def hipcc():
 
 
 def build(extra=()):
-    cmd = [hipcc()] + HIPCC_FLAGS + list(extra) + ["-o", LIB] + \
-        [os.path.join(SRC, s) for s in SOURCES]
-    subprocess.check_call(cmd)
+    cmds = [[hipcc()] + HIPCC_FLAGS + list(extra) + ["-o", out] + [os.path.join(SRC, s) for s in srcs]
+            for out, srcs in ((LIB, SOURCES), (CEIL_LIB, CEIL_SOURCES))]
+    procs = [subprocess.Popen(c) for c in cmds]
+    for p, c in zip(procs, cmds):
+        if p.wait() != 0:
+            raise subprocess.CalledProcessError(p.returncode, c)
     return LIB
 
 

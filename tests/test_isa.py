@@ -21,7 +21,7 @@ sys.path.insert(0, ROOT)
 
 from paper_2608_00455_amd import build as B  # noqa: E402
 
-SOURCES = ["extract.hip", "remap.hip", "store.hip"]
+SOURCES = ["extract.hip", "remap.hip", "store.hip", "ceilings.hip"]
 
 
 def _hipcc_ok():

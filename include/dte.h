@@ -40,7 +40,8 @@ typedef int32_t dte_status;
 #define DTE_OK 0
 #define DTE_ERR_ARG 1      /* invalid argument (null pointer, bad size, bad hyperparameter) */
 #define DTE_ERR_PLAN 2     /* transfer plan failed validation */
-#define DTE_ERR_CAPACITY 3 /* reserved: output capacity exceeded (reported via counters) */
+#define DTE_ERR_CAPACITY 3 /* a capacity beyond dte_ordered_noalloc_max_capacity(); overflow of
+                             output buffers is reported through the counters instead */
 #define DTE_ERR_HIP 4      /* a HIP runtime call failed */
 #define DTE_ERR_IO 5       /* a file could not be read or written (dte_store.h) */
 #define DTE_ERR_CORRUPT 6  /* stored data failed its checksum or format check */
@@ -162,6 +163,31 @@ dte_status dte_extract_delta_ordered(const float* p, const float* m, const float
                                      int64_t* out_idx, uint16_t* out_val, int64_t capacity,
                                      int64_t* cursor, void* workspace, int64_t workspace_bytes,
                                      float* out_prev, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * ordered call of dte_extract_delta_ordered with its workspace in a static
+ * array of 64 MiB that the library holds on every device it runs on until
+ * the process ends, so the call needs no workspace argument and allocates
+ * nothing (no hipMalloc, no hipFree, no allocating library routine).
+ * Arguments, results, order and cursor semantics are those of
+ * dte_extract_delta_ordered.  The array is shared by every call on one
+ * device and keeps the last call's contents; calls that overlap on one
+ * device (several streams or host threads) race and must be serialised by
+ * the caller.
+ * capacity: at most dte_ordered_noalloc_max_capacity() (about 3.3 million
+ *           entries), else DTE_ERR_CAPACITY and nothing is enqueued.
+ * Errors: as dte_extract_delta; DTE_ERR_CAPACITY; DTE_ERR_HIP also when the
+ * array's device address cannot be obtained. */
+dte_status dte_extract_delta_ordered_noalloc(const float* p, const float* m, const float* v,
+                                             int64_t n, int64_t index_base,
+                                             const dte_adamw_step* hp, int64_t* out_idx,
+                                             uint16_t* out_val, int64_t capacity,
+                                             int64_t* cursor, float* out_prev, void* stream);
+
+/* Host-only.  The largest capacity dte_extract_delta_ordered_noalloc
+ * accepts. */
+int64_t dte_ordered_noalloc_max_capacity(void);
 
 /* One canonical parameter of the flat trainer shard (paper sec. 4.2.2:
  * sender-local converted tensor of shape n_s): flat_begin is its offset in

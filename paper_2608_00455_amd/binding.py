@@ -17,7 +17,8 @@ DTE_MAX_DIMS = 4
 DTE_MAX_RANKS = 64
 
 EXPORTED = ("dte_derive_scalars", "dte_extract_delta", "dte_ordered_workspace_bytes",
-            "dte_extract_delta_ordered", "dte_plan_create", "dte_plan_destroy",
+            "dte_extract_delta_ordered", "dte_extract_delta_ordered_noalloc",
+            "dte_ordered_noalloc_max_capacity", "dte_plan_create", "dte_plan_destroy",
             "dte_plan_info", "dte_remap", "dte_extract_remap", "dte_apply", "dte_adamw_forward",
             "dte_status_string")
 
@@ -83,6 +84,12 @@ def _lib():
         L.dte_extract_delta_ordered.argtypes = [P, P, P, I64, I64,
                                                 ctypes.POINTER(dte_adamw_step), P, P, I64, P, P,
                                                 I64, P, P]
+        L.dte_extract_delta_ordered_noalloc.restype = S
+        L.dte_extract_delta_ordered_noalloc.argtypes = [P, P, P, I64, I64,
+                                                        ctypes.POINTER(dte_adamw_step), P, P,
+                                                        I64, P, P, P]
+        L.dte_ordered_noalloc_max_capacity.restype = I64
+        L.dte_ordered_noalloc_max_capacity.argtypes = []
         L.dte_plan_create.restype = S
         L.dte_plan_create.argtypes = [ctypes.POINTER(dte_segment), I32, ctypes.POINTER(dte_op),
                                       I32, I32, ctypes.POINTER(I64), ctypes.POINTER(P)]
@@ -156,6 +163,19 @@ def dte_extract_delta_ordered(p, m, v, n, index_base, hp, out_idx, out_val, capa
                                             out_idx, out_val, capacity, cursor,
                                             workspace or None, workspace_bytes,
                                             out_prev or None, stream or None))
+
+
+def dte_extract_delta_ordered_noalloc(p, m, v, n, index_base, hp, out_idx, out_val, capacity,
+                                      cursor, out_prev=0, stream=0):
+    _check("dte_extract_delta_ordered_noalloc",
+           _lib().dte_extract_delta_ordered_noalloc(p, m, v, n, index_base,
+                                                    ctypes.byref(_hp(hp)), out_idx, out_val,
+                                                    capacity, cursor, out_prev or None,
+                                                    stream or None))
+
+
+def dte_ordered_noalloc_max_capacity() -> int:
+    return int(_lib().dte_ordered_noalloc_max_capacity())
 
 
 def dte_extract_remap(p, m, v, n, index_base, hp, plan, out_off, out_val, rank_capacity,

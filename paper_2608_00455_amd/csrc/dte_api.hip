@@ -368,6 +368,9 @@ struct OrderedWorkspace {
 
 int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
+// Bytes of the static workspace of dte_extract_delta_ordered_noalloc.
+constexpr int64_t kNoallocBytes = (int64_t)64 << 20;
+
 OrderedWorkspace ordered_layout(int64_t capacity)
 {
     OrderedWorkspace w;
@@ -408,23 +411,18 @@ int64_t dte_ordered_workspace_bytes(int64_t capacity)
     return ordered_layout(capacity).total;
 }
 
-dte_status dte_extract_delta_ordered(const float* p, const float* m, const float* v, int64_t n,
-                                     int64_t index_base, const dte_adamw_step* hp,
-                                     int64_t* out_idx, uint16_t* out_val, int64_t capacity,
-                                     int64_t* cursor, void* workspace, int64_t workspace_bytes,
-                                     float* out_prev, void* stream)
+namespace {
+
+// The ordered call on a workspace of workspace_bytes at `workspace`
+// (device, 256-byte aligned, at least dte_ordered_workspace_bytes(capacity)).
+dte_status extract_ordered(const float* p, const float* m, const float* v, int64_t n,
+                           int64_t index_base, const dte_adamw_step* hp, int64_t* out_idx,
+                           uint16_t* out_val, int64_t capacity, int64_t* cursor, void* workspace,
+                           float* out_prev, hipStream_t s)
 {
-    if (!extract_args_ok(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cursor))
-        return DTE_ERR_ARG;
-    if (n == 0) return DTE_OK;
-    const int64_t need = dte_ordered_workspace_bytes(capacity);
-    if (need < 0 || !workspace || workspace_bytes < need ||
-        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-        return DTE_ERR_ARG;
     const OrderedWorkspace w = ordered_layout(capacity);
     char* base = static_cast<char*>(workspace);
     int64_t* counters = reinterpret_cast<int64_t*>(base + w.counters);
-    const hipStream_t s = (hipStream_t)stream;
     const int cus = current_cus();
     // unordered fill level and run count start at zero (a fill kernel)
     if (dte::launch_zero_i64(counters, 2, s) != hipSuccess) return DTE_ERR_HIP;
@@ -461,6 +459,82 @@ dte_status dte_extract_delta_ordered(const float* p, const float* m, const float
     o.capacity = capacity;
     o.cursor = cursor;
     return dte::launch_order(o, cus, s) == hipSuccess ? DTE_OK : DTE_ERR_HIP;
+}
+
+}  // namespace
+
+dte_status dte_extract_delta_ordered(const float* p, const float* m, const float* v, int64_t n,
+                                     int64_t index_base, const dte_adamw_step* hp,
+                                     int64_t* out_idx, uint16_t* out_val, int64_t capacity,
+                                     int64_t* cursor, void* workspace, int64_t workspace_bytes,
+                                     float* out_prev, void* stream)
+{
+    if (!extract_args_ok(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cursor))
+        return DTE_ERR_ARG;
+    if (n == 0) return DTE_OK;
+    const int64_t need = dte_ordered_workspace_bytes(capacity);
+    if (need < 0 || !workspace || workspace_bytes < need ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return DTE_ERR_ARG;
+    return extract_ordered(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cursor,
+                           workspace, out_prev, (hipStream_t)stream);
+}
+
+// ---- the ordered call without allocation ---------------------------------
+
+// Its workspace: one array per device in the code object's own storage,
+// held while the library is loaded.  Host code never uses this name as an
+// address (it is a host-side stand-in); the device address comes from
+// hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[kNoallocBytes];
+
+namespace {
+
+// Device address of `scratch` on the current device (nullptr if it cannot
+// be obtained).  Threads racing on the first call both store the same value.
+void* scratch_address()
+{
+    static std::atomic<void*> cache[64];
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    void* ptr = cache[dev].load(std::memory_order_acquire);
+    if (ptr == nullptr) {
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+        cache[dev].store(ptr, std::memory_order_release);
+    }
+    return ptr;
+}
+
+}  // namespace
+
+int64_t dte_ordered_noalloc_max_capacity(void)
+{
+    // the largest capacity whose workspace fits (the size grows with it)
+    int64_t lo = 0, hi = kNoallocBytes;
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo + 1) / 2;
+        if (ordered_layout(mid).total <= kNoallocBytes)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+dte_status dte_extract_delta_ordered_noalloc(const float* p, const float* m, const float* v,
+                                             int64_t n, int64_t index_base,
+                                             const dte_adamw_step* hp, int64_t* out_idx,
+                                             uint16_t* out_val, int64_t capacity,
+                                             int64_t* cursor, float* out_prev, void* stream)
+{
+    if (!extract_args_ok(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cursor))
+        return DTE_ERR_ARG;
+    if (capacity > dte_ordered_noalloc_max_capacity()) return DTE_ERR_CAPACITY;
+    if (n == 0) return DTE_OK;
+    void* ws = scratch_address();
+    if (ws == nullptr) return DTE_ERR_HIP;
+    return extract_ordered(p, m, v, n, index_base, hp, out_idx, out_val, capacity, cursor, ws,
+                           out_prev, (hipStream_t)stream);
 }
 
 dte_status dte_adamw_forward(float* p, float* m, float* v, const float* g, int64_t n,

@@ -90,6 +90,21 @@ def test_argument_errors_and_empty_calls():
     assert "ERR_PLAN" in B.dte_status_string(B.DTE_ERR_PLAN)
 
 
+def test_noalloc_capacity_limit():
+    """The no-allocation ordered call takes capacities whose workspace fits
+    its 64 MiB static array and rejects larger ones before any device work."""
+    cap = B.dte_ordered_noalloc_max_capacity()
+    assert B.dte_ordered_workspace_bytes(cap) <= 64 << 20 < B.dte_ordered_workspace_bytes(cap + 1)
+    assert cap > 3_000_000
+    hp = B.dte_adamw_step(1e-6, 0.9, 0.999, 1e-8, 0.01, 100)
+    call = lambda *a: B.raw_status("dte_extract_delta_ordered_noalloc", *a)  # noqa: E731
+    assert call(16, 16, 16, 4, 0, ctypes.byref(hp), 16, 16, cap + 1, 16, None,
+                None) == B.DTE_ERR_CAPACITY
+    assert call(16, 16, 16, -1, 0, ctypes.byref(hp), 16, 16, 4, 16, None, None) == B.DTE_ERR_ARG
+    assert call(None, None, None, 0, 0, ctypes.byref(hp), None, None, 0, None, None,
+                None) == B.DTE_OK
+
+
 def test_every_status_code_has_its_own_name():
     codes = [B.DTE_OK, B.DTE_ERR_ARG, B.DTE_ERR_PLAN, B.DTE_ERR_CAPACITY, B.DTE_ERR_HIP,
              B.DTE_ERR_IO, B.DTE_ERR_CORRUPT, B.DTE_ERR_CHAIN, B.DTE_ERR_UNSUPPORTED,

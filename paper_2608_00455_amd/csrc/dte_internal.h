@@ -102,7 +102,7 @@ struct ExtractParams {
 constexpr int kMaxOrderedWaves = 16384;
 // Entries a wave stages before it flushes them: every flush but a wave's
 // last holds exactly this many (the ordered workspace is sized with it).
-constexpr int kWaveStage = 1024;
+constexpr int kWaveStage = 1536;
 
 // Launches the extract kernels; *waves receives the number of waves
 // launched (the global wave numbers are 0 .. *waves - 1).

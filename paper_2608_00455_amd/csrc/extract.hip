@@ -223,6 +223,26 @@ __device__ __forceinline__ void write_out(const ExtractParams& a, const WaveStag
     }
 }
 
+// Write a wave's staged entries (so.staged > 0) to positions base, base + 1,
+// ...  A wave that has so far found more than one changed element per
+// kDenseRatio elements scanned writes its offsets with non-temporal stores
+// (measured faster on deltas of several percent of the state, slower on
+// sparse ones); the choice is wave-uniform.
+__device__ __forceinline__ void write_staged(const ExtractParams& a, const WaveStage& st,
+                                             Staging& so, int64_t base, int lane)
+{
+    const int staged = so.staged;
+    const uint32_t last = __builtin_amdgcn_readfirstlane(st.key[staged - 1]);
+    const int64_t scanned = ((int64_t)(last >> kTileBits) + 1) * kWaveTile;
+    if ((so.flushed + staged) * kDenseRatio > scanned)
+        write_out<true>(a, st, base, staged, lane);
+    else
+        write_out<false>(a, st, base, staged, lane);
+    so.flushed += staged;
+    so.staged = 0;
+    wave_sync();   // the staging area is rewritten next: finish these reads first
+}
+
 // Copy a wave's staged LDS entries to the reserved global range (and, in
 // ordered mode, record the run).  Routing mode: route them through the plan
 // into the receiver buckets instead (count, one reservation per rank, write).
@@ -306,19 +326,7 @@ __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging&
         }
     }
     base = __shfl(base, 0);
-    // a wave that has so far found more than one changed element per
-    // kDenseRatio elements scanned writes its offsets with non-temporal
-    // stores (measured faster on deltas of several percent of the state,
-    // slower on sparse ones); the choice is wave-uniform
-    const uint32_t last = __builtin_amdgcn_readfirstlane(st.key[staged - 1]);
-    const int64_t scanned = ((int64_t)(last >> kTileBits) + 1) * kWaveTile;
-    if ((so.flushed + staged) * kDenseRatio > scanned)
-        write_out<true>(a, st, (int64_t)base, staged, lane);
-    else
-        write_out<false>(a, st, (int64_t)base, staged, lane);
-    so.flushed += staged;
-    so.staged = 0;
-    wave_sync();   // the staging area is rewritten next: finish these reads first
+    write_staged(a, st, so, (int64_t)base, lane);
 }
 
 // Selection of the four elements of each lane's float4 slot (256
@@ -380,6 +388,40 @@ __device__ __forceinline__ void stage_changed(const ExtractParams& a, const Wave
         st.val[pos - kWaveStage] = val;
     }
     so.staged = before + cnt - kWaveStage;
+}
+
+// Combined flushes of the unordered call.  Every kRound tiles, and once at
+// the end, the four waves of a block meet at a barrier; when they hold at
+// least kBlockFlush staged entries (at the end: any), one atomicAdd on the
+// cursor reserves room for all of them and each wave writes its entries
+// after those of the waves before it.  Every wave of the device reserving
+// its own space from the one cursor address is what slows the stream (the
+// atomics, not the stores), so fewer, larger reservations are the point; a
+// wave whose staging area fills between two meetings still flushes on its
+// own.  Block-uniform control flow; the two LDS slots alternate, so a slot
+// is rewritten only after every wave has passed a later barrier.
+constexpr int kRound = 4;
+constexpr int kBlockFlush = 3 * 1024;
+
+__device__ void block_round(const ExtractParams& a, const WaveStage& st, Staging& so, int lane,
+                            int wave, int (*s_cnt)[kWaves], unsigned long long* s_base, int slot,
+                            bool last_round)
+{
+    if (lane == 0) s_cnt[slot][wave] = so.staged;
+    __syncthreads();
+    int total = 0, before = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const int c = s_cnt[slot][w];
+        total += c;
+        before += w < wave ? c : 0;
+    }
+    if (total == 0 || (!last_round && total < kBlockFlush)) return;
+    if (threadIdx.x == 0)
+        s_base[slot] = atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor),
+                                 (unsigned long long)total);
+    __syncthreads();
+    if (so.staged > 0) write_staged(a, st, so, (int64_t)s_base[slot] + before, lane);
 }
 
 // Exact inverse of every queued candidate, 64 per pass; changed ones are
@@ -537,6 +579,8 @@ __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_
     __shared__ float s_qm[kWaves][kQueue];
     __shared__ float s_qv[kWaves][kQueue];
     __shared__ uint32_t s_qkey[kWaves][kQueue];
+    __shared__ int s_cnt[2][kWaves];
+    __shared__ unsigned long long s_base[2];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -549,16 +593,26 @@ __global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_
     Staging so{0, 0, 0, 0};
     const WaveStage st{s_key[wave], s_val[wave], s_qp[wave], s_qm[wave], s_qv[wave],
                        s_qkey[wave], w_first, a.wave0 + (int32_t)g};
-    uint32_t iter = 0;
+    // unordered output: combined flushes (block_round); every wave of the
+    // block runs the same `per` iterations, so the barriers match
+    const bool combine = !kRoute && a.runs == nullptr;
     int queued = 0;
-    for (int64_t t = w_first; t < w_last; ++t) {
-        f32x4 P[kVec], M[kVec], V[kVec];
-        load_tile<kFull, kVecLoads>(a, t * kWaveTile, lane, P, M, V);
-        process_tile<kFull, kVecLoads, kDecayOne, kWritePrev, kLit, kRoute>(a, t * kWaveTile, lane, so,
-                                                             queued, st, iter++, P, M, V);
+    for (int64_t it = 0; it < per; ++it) {
+        const int64_t t = w_first + it;
+        if (t < w_last) {
+            f32x4 P[kVec], M[kVec], V[kVec];
+            load_tile<kFull, kVecLoads>(a, t * kWaveTile, lane, P, M, V);
+            process_tile<kFull, kVecLoads, kDecayOne, kWritePrev, kLit, kRoute>(
+                a, t * kWaveTile, lane, so, queued, st, (uint32_t)it, P, M, V);
+        }
+        if (combine && it % kRound == kRound - 1)
+            block_round(a, st, so, lane, wave, s_cnt, s_base, (int)((it / kRound) & 1), false);
     }
     if (queued > 0) drain_queue<kDecayOne, kLit, kRoute>(a, st, queued, so, lane);
-    if (so.staged > 0) flush_wave<kRoute>(a, st, so, lane);
+    if (combine)
+        block_round(a, st, so, lane, wave, s_cnt, s_base, (int)((per / kRound) & 1), true);
+    else if (so.staged > 0)
+        flush_wave<kRoute>(a, st, so, lane);
     if (a.runs && lane == 0) {
         a.wave_count[st.wave] = so.flushed;
         a.region_count[st.wave] = so.in_region;

@@ -192,9 +192,10 @@ __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     // slices start on group (else chunk) boundaries when each block gets
-    // several: no group is left partly empty, and since extract flushes
-    // whole 1024-entry runs a chunk then lies in one run (usually one
-    // segment); small deltas are split evenly instead
+    // several: no group is left partly empty, and since extract writes each
+    // wave's entries in ascending runs of hundreds to thousands, a chunk
+    // then usually lies in one run (one segment); small deltas are split
+    // evenly instead
     // blocks in use: about kBlockEntries entries each, more (at least
     // kMinBlockEntries each) up to `fill` blocks, at most the grid
     int64_t g = (total + kBlockEntries - 1) / kBlockEntries;

@@ -240,9 +240,6 @@ def main():
     ap.add_argument("--lr", type=float, default=None)
     ap.add_argument("--literal", action="store_true",
                     help="literal operation order of the AdamW inverse (four divisions)")
-    ap.add_argument("--fused", action="store_true",
-                    help="dte_extract_remap (detection routed straight into the buckets) "
-                         "instead of dte_extract_delta + dte_remap")
     ap.add_argument("--ordered", action="store_true",
                     help="dte_extract_delta_ordered (ascending, deterministic delta)")
     ap.add_argument("--norm-group", action="store_true",
@@ -339,27 +336,15 @@ def main():
             pipe.apply()
             rec(4)
             return
-        if args.fused:
-            pipe.cursor.zero_()
-            pipe.rank_count.zero_()
-            rec(1)
-            for b, e, h in runs:
-                if len(runs) == 1:
-                    pipe.extract_remap(p, m, v, h)
-                else:
-                    pipe.extract_remap(p[b:e], m[b:e], v[b:e], h, n=e - b, index_base=b)
-            rec(2)
-            rec(3)
+        pipe.reset()
+        rec(1)
+        if len(runs) == 1:
+            pipe.extract(p, m, v, hp)
         else:
-            pipe.reset()
-            rec(1)
-            if len(runs) == 1:
-                pipe.extract(p, m, v, hp)
-            else:
-                pipe.extract_runs(p, m, v, runs)
-            rec(2)
-            pipe.remap()
-            rec(3)
+            pipe.extract_runs(p, m, v, runs)
+        rec(2)
+        pipe.remap()
+        rec(3)
         pipe.apply()
         rec(4)
 
@@ -405,23 +390,18 @@ def main():
         kernel = "apply"
     else:
         k = ext
-        if args.fused:                        # read theta, m, v; write (offset, value) per route
-            k_bytes = 12 * n + 10 * routed
-        else:                                 # read theta, m, v; write (idx, val)
-            k_bytes = 12 * n + 10 * changed
+        k_bytes = 12 * n + 10 * changed       # read theta, m, v; write (idx, val)
         value = n / (ms_step / 1e3)
         metric_unit = "elements/s"
-        kernel = "extract_remap" if args.fused else "extract"
+        kernel = "extract"
     if apply_only:
         step_bytes = k_bytes
-    elif args.fused:
-        step_bytes = 12 * n + 10 * routed + 12 * routed
     else:
         step_bytes = 12 * n + 10 * changed + 10 * changed + 10 * routed + 12 * routed
     achieved = k_bytes / (k["mean"] / 1e3) / 1e9
     # the counters were taken for the default configuration only (folded
     # order, unordered output, one parameter group)
-    default_mode = not (args.ordered or args.fused or args.literal or args.norm_group)
+    default_mode = not (args.ordered or args.literal or args.norm_group)
     out = {
         "metric": "delta-extract+remap+apply: elements/s and HBM GB/s (% of peak), "
                   "Qwen3-8B shape",
@@ -438,7 +418,7 @@ def main():
         "data": "synthetic (seeded Philox draws, one AdamW step on the device)",
         "config": {"workload": wl.name, "elements": n, "changed": changed,
                    "extract_calls": len(runs), "settle_s": settle, "ordered": ordered,
-                   "fused": bool(args.fused), "order": "literal" if args.literal else "folded",
+                   "order": "literal" if args.literal else "folded",
                    "change_fraction": c, "receiver_ranks": len(counts),
                    "routed_entries": routed, "lr": hp.lr,
                    "step_algorithmic_bytes": step_bytes,

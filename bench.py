@@ -258,8 +258,8 @@ def main():
                          "occupy less than 2 GB, so that they cannot stay in the 256 MB "
                          "last-level cache between steps; else 0)")
     ap.add_argument("--settle", type=float, default=15.0, metavar="SECONDS",
-                    help="wait before allocating the state (less the time of the CPU "
-                         "baseline, which runs first): device memory that a process "
+                    help="wait before allocating the state (after the CPU baseline, which "
+                         "runs first): device memory that a process "
                          "released moments earlier is handed out in less contiguous pieces "
                          "until the driver has reclaimed it, which slows streaming kernels")
     ap.add_argument("--store", default=None, metavar="DIR",
@@ -301,7 +301,7 @@ def main():
     if args.literal:
         hp = type(hp)(lr=hp.lr, beta1=hp.beta1, beta2=hp.beta2, eps=hp.eps,
                       weight_decay=hp.weight_decay, step=hp.step, order=W.ORDER_LITERAL)
-    settle = max(0.0, args.settle - cpu_s)
+    settle = args.settle
     if settle > 0:
         log("bench: settling %.0f s before allocating" % settle)
         time.sleep(settle)

@@ -24,7 +24,7 @@
 // Apply: shard[off] = val; each lane keeps eight independent
 // load-then-store chains in flight (the scattered 2-byte stores are
 // read-modify-write at the memory side, so parallelism is what matters);
-// ranks with dense updates store past the cache.
+// ranks with dense updates or shards larger than 1 GiB store past the cache.
 #include <hip/hip_runtime.h>
 
 #include "dte_internal.h"
@@ -240,6 +240,7 @@ __global__ __launch_bounds__(kBlock) void remap_kernel(PlanView pl, const int64_
 
 constexpr int kApplyUnroll = 8;
 constexpr int64_t kDenseApply = 64;
+constexpr int64_t kCachedApplyBytes = (int64_t)1 << 30;
 
 __global__ __launch_bounds__(kBlock) void apply_kernel(ApplySlice s,
                                                       const int64_t* __restrict__ rank_count)
@@ -254,9 +255,11 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(ApplySlice s,
         uint16_t* shard = s.shard[r];
         const int64_t numel = s.numel[r];
         // a rank that receives more than one entry per kDenseApply shard
-        // elements takes non-temporal stores: sparser updates gain from
-        // the cache's write-back, denser ones measured faster without it
-        const bool stream = n * kDenseApply > numel;
+        // elements, or whose shard is larger than kCachedApplyBytes, takes
+        // non-temporal stores: sparse updates of a shard that the caches
+        // can hold gain from their write-back, denser ones and larger
+        // shards measured faster without it
+        const bool stream = n * kDenseApply > numel || numel * 2 > kCachedApplyBytes;
         for (int64_t e0 = t; e0 < n; e0 += nthreads * kApplyUnroll) {
             int64_t j[kApplyUnroll];
             uint16_t v[kApplyUnroll];

@@ -52,4 +52,25 @@ def test_traffic_record_lookup(path):
 
 def test_traffic_is_withheld_for_another_mode_or_workload():
     assert bench.measured_traffic("qwen3_8b_tp4", "extract", "no such mode") is None
-    assert bench.measured_traffic("tiny_block_tp2", "extract", "unordered") is None
+    assert bench.measured_traffic("no_such_workload", "extract", "unordered") is None
+
+
+APPLY_RECORDS = sorted(glob.glob(os.path.join(ROOT, "profiles", "apply_*_traffic.json")))
+
+
+@pytest.mark.parametrize("path", APPLY_RECORDS, ids=[os.path.basename(p) for p in APPLY_RECORDS])
+def test_apply_traffic_record_lookup(path):
+    """Apply-only records: the lookup returns the recorded bytes while the
+    built apply kernel is the profiled one; scattered 2-byte stores cost
+    whole sectors, so the bytes exceed the algorithmic ones."""
+    from paper_2608_00455_amd import devcode
+    rec = json.load(open(path))
+    workload = os.path.basename(path)[len("apply_"):-len("_traffic.json")]
+    got = bench.measured_traffic(workload, "apply", rec["mode"])
+    lib = os.path.join(ROOT, rec["library"])
+    if not os.path.exists(lib) or \
+            devcode.kernel_sha256(lib, rec["kernel_symbols"]) != rec["device_code_sha256"]:
+        assert got is None
+        return
+    assert got == rec["traffic_bytes_per_launch"]
+    assert got > rec["algorithmic_bytes_per_launch"]

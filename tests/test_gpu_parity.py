@@ -564,3 +564,39 @@ def test_ordered_extract_when_waves_outgrow_their_regions(slack):
         # counters (entries, runs); both paths were taken
         shared_entries, shared_runs = ws[-256:-240].cpu().numpy().view(np.int64).tolist()
         assert shared_runs > 0 and 0 < shared_entries < idx.size
+
+
+@pytest.mark.parametrize("lr", [1e-3, 1e-2])
+def test_dense_delta_spanning_many_rounds(lr):
+    """A 38M-element model at a learning rate where most elements change:
+    every wave scans several tiles and stages far more than its area holds
+    between two meetings of its block, so the unordered call mixes
+    combined reservations with flushes of single waves; the ordered call
+    and the remap follow.  Everything equals the oracle."""
+    wl = W.scaled_dense(layers=2, tp=2, hidden=1024, heads_q=8, heads_kv=2, head_dim=128,
+                        intermediate=4096, vocab=4096, lr=lr)
+    say("case: dense delta", wl.name, wl.numel, lr)
+    res = orun.extract(wl)
+    assert res.idx.size > wl.numel // 4
+    p, m, v = generate_state(wl)
+    spec = layouts.build_spec(wl)
+    for ordered in (False, True):
+        pipe = DeltaPipeline(spec, capacity=wl.numel, ordered=ordered)
+        pipe.reset()
+        pipe.extract(p, m, v, wl.hp)
+        pipe.remap()
+        sync()
+        if ordered:
+            idx, val, total = pipe.delta(raw=True)
+            assert total == res.idx.size
+            assert np.array_equal(idx, res.idx) and np.array_equal(val, res.val)
+        else:
+            assert_delta_equal(pipe, res)
+        buckets, counts = pipe.buckets()
+        want = oremap.remap(oplan.build_plan(wl), res.idx, res.val)
+        for r in range(len(want)):
+            assert np.array_equal(buckets[r][0], want[r][0]), r
+            assert np.array_equal(buckets[r][1], want[r][1]), r
+        pipe.close()
+    del p, m, v
+    torch.cuda.empty_cache()

@@ -97,13 +97,18 @@ def measured_traffic(workload_name, kernel, mode):
     return rec["traffic_bytes_per_launch"]
 
 
-def ceilings(p, m, v, pipe, stream, reps=5):
+def ceilings(p, m, v, pipe, stream, entries, reps=5):
     """Second denominators measured on the same GPU and buffers: the rate of
     a plain read of theta, m, v (12 bytes per element, extract's access
-    pattern, no arithmetic, no stores; best of 2, 3 and 4 blocks per CU) and
-    the time of writing whole 64-byte lines at every apply address of the
-    step's buckets (into scratch buffers of the shards' size; best of 4, 8
-    and 16 blocks per CU)."""
+    pattern, no arithmetic, no stores; best of 2, 3 and 4 blocks per CU);
+    the writes of an `entries`-entry delta alone (8-byte offsets and 2-byte
+    values spread evenly over the tiles, into the pipeline's delta buffers,
+    which the step has finished with; same block counts), whose time added
+    to the read's bounds any kernel that moves extract's bytes, and the
+    same writes issued together with the read (a naive mix); and the time of
+    writing whole 64-byte lines at every apply address of the step's
+    buckets (into scratch buffers of the shards' size; best of 4, 8 and 16
+    blocks per CU)."""
     import ctypes
 
     import torch
@@ -116,6 +121,10 @@ def ceilings(p, m, v, pipe, stream, reps=5):
     lib.ceil_read3_waves.argtypes = [I32]
     lib.ceil_read3.restype = ctypes.c_int
     lib.ceil_read3.argtypes = [P, P, P, I64, I32, P, P]
+    lib.ceil_read3_write.restype = ctypes.c_int
+    lib.ceil_read3_write.argtypes = [P, P, P, I64, I64, P, P, I32, P, P]
+    lib.ceil_write_entries.restype = ctypes.c_int
+    lib.ceil_write_entries.argtypes = [I64, P, P, I32, P]
     lib.ceil_line_writes.restype = ctypes.c_int
     lib.ceil_line_writes.argtypes = [I32, P, P, P, P, P, I32, P]
     s = stream.cuda_stream
@@ -146,6 +155,24 @@ def ceilings(p, m, v, pipe, stream, reps=5):
         del sink
     out["read_stream"] = {"gbs": 12 * n / (best[0] / 1e3) / 1e9, "ms": best[0],
                           "blocks_per_cu": best[1], "bytes": 12 * n}
+    e = min(entries, pipe.capacity)
+    if e > 0:
+        rd = best[0]
+        wr = mix = None
+        for bpc in (2, 3, 4):
+            sink = torch.zeros(64 * lib.ceil_read3_waves(bpc), dtype=torch.int32, device="cuda")
+            ms = timed(lambda: lib.ceil_write_entries(e, pipe.idx.data_ptr(), pipe.val.data_ptr(),
+                                                      bpc, s), "ceil_write_entries")
+            wr = ms if wr is None or ms < wr else wr
+            ms = timed(lambda: lib.ceil_read3_write(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, e,
+                                                    pipe.idx.data_ptr(), pipe.val.data_ptr(), bpc,
+                                                    sink.data_ptr(), s), "ceil_read3_write")
+            mix = ms if mix is None or ms < mix else mix
+            del sink
+        b = 12 * n + 10 * e
+        out["read_then_write"] = {"ms": rd + wr, "read_ms": rd, "write_ms": wr,
+                                  "gbs": b / ((rd + wr) / 1e3) / 1e9, "bytes": b, "entries": e,
+                                  "naive_mix_ms": mix}
     R = len(pipe.shards)
     if R <= 16:
         scratch = [torch.empty_like(t) for t in pipe.shards]
@@ -442,10 +469,12 @@ def main():
         torch.cuda.empty_cache()
     if not args.no_ceilings:
         log("bench: reference read stream and scattered lines")
-        ce = ceilings(p, m, v, pipe, stream)
+        ce = ceilings(p, m, v, pipe, stream, 0 if apply_only else changed)
         rs = ce["read_stream"]
         if kernel == "extract":
             rs["kernel_frac"] = achieved / rs["gbs"]
+            if "read_then_write" in ce:
+                ce["read_then_write"]["kernel_frac"] = ce["read_then_write"]["ms"] / k["mean"]
         if "apply_scattered_lines" in ce:
             ce["apply_scattered_lines"]["apply_ms"] = app["mean"]
             ce["apply_scattered_lines"]["apply_frac"] = \

@@ -8,6 +8,15 @@
 //    (persistent grid, each wave a contiguous range of 2048-element tiles,
 //    eight 16-byte non-temporal loads per lane and array in flight) with no
 //    arithmetic beyond folding the loaded bits, and no stores;
+//  - ceil_read3_write: the same read, plus the output extraction writes
+//    for a delta of a given size: 8-byte offsets (non-temporal stores) and
+//    2-byte values, spread evenly over the tiles, each wave writing its
+//    tiles' share contiguously, with no atomics, no selection and nothing
+//    else: the read and write mix that extraction's bytes make, issued
+//    naively; ceil_write_entries: the same entries written alone, each wave
+//    one contiguous range.  A read stream and a write stream, one after the
+//    other, bound any kernel that moves extraction's bytes over the one
+//    memory bus;
 //  - ceil_line_writes: for every bucket entry of every rank, a whole 64-byte
 //    line written at the line that holds the entry's element (four 16-byte
 //    stores), into a buffer of the shard's size: the rate of scattered
@@ -57,6 +66,64 @@ __global__ __launch_bounds__(kBlock) void read3_kernel(const float* __restrict__
     // a store the compiler cannot rule out keeps the loads; it practically
     // never happens
     if (acc == 0x9E3779B9u) sink[g * 64 + lane] = acc;
+}
+
+// read3_kernel plus, for tile t, entries [E t / tiles, E (t+1) / tiles) of
+// out_idx / out_val written (values independent of the loads, so that the
+// stores wait for nothing).
+__global__ __launch_bounds__(kBlock) void read3_write_kernel(const float* __restrict__ a,
+                                                             const float* __restrict__ b,
+                                                             const float* __restrict__ c,
+                                                             int64_t tiles, int64_t entries,
+                                                             int64_t* __restrict__ out_idx,
+                                                             uint16_t* __restrict__ out_val,
+                                                             uint32_t* __restrict__ sink)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t g = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+    const int64_t nw = (int64_t)gridDim.x * kWaves;
+    const int64_t per = (tiles + nw - 1) / nw;
+    const int64_t first = g * per;
+    const int64_t last = first + per < tiles ? first + per : tiles;
+    uint32_t acc = 0;
+    for (int64_t t = first; t < last; ++t) {
+        f32x4 A[kVec], B[kVec], C[kVec];
+#pragma unroll
+        for (int j = 0; j < kVec; ++j) {
+            const int64_t e = t * kTile + (int64_t)(j * 64 + lane) * 4;
+            A[j] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a + e));
+            B[j] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(b + e));
+            C[j] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(c + e));
+        }
+        const int64_t e0 = entries * t / tiles, e1 = entries * (t + 1) / tiles;
+        for (int64_t e = e0 + lane; e < e1; e += 64) {
+            __builtin_nontemporal_store(t * kTile + (e - e0), out_idx + e);
+            out_val[e] = (uint16_t)e;
+        }
+#pragma unroll
+        for (int j = 0; j < kVec; ++j) {
+            const u32x4 x = __builtin_bit_cast(u32x4, A[j]) ^ __builtin_bit_cast(u32x4, B[j]) ^
+                            __builtin_bit_cast(u32x4, C[j]);
+            acc ^= x.x ^ x.y ^ x.z ^ x.w;
+        }
+    }
+    if (acc == 0x9E3779B9u) sink[g * 64 + lane] = acc;
+}
+
+// Entries [E g / waves, E (g+1) / waves) of out_idx / out_val written by
+// wave g, 64 at a time.
+__global__ __launch_bounds__(kBlock) void write_entries_kernel(int64_t entries,
+                                                               int64_t* __restrict__ out_idx,
+                                                               uint16_t* __restrict__ out_val)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t g = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
+    const int64_t nw = (int64_t)gridDim.x * kWaves;
+    const int64_t e1 = entries * (g + 1) / nw;
+    for (int64_t e = entries * g / nw + lane; e < e1; e += 64) {
+        __builtin_nontemporal_store(e, out_idx + e);
+        out_val[e] = (uint16_t)e;
+    }
 }
 
 constexpr int kMaxRanks = 16;
@@ -140,6 +207,49 @@ int ceil_read3(const float* a, const float* b, const float* c, int64_t n, int32_
     const dim3 grid((unsigned)(cus_of_current() * blocks_per_cu));
     hipLaunchKernelGGL(read3_kernel, grid, dim3(kBlock), 0, (hipStream_t)stream, a, b, c, tiles,
                        sink);
+    return hipGetLastError() == hipSuccess ? 0 : 4;
+}
+
+// ceil_read3 plus writes of `entries` (offset, value) pairs to out_idx[0,
+// entries) and out_val[0, entries) (device; out_idx 8-byte aligned), spread
+// evenly over the tiles.  The written values are meaningless.  Returns 0, 1
+// on a bad argument, 4 on a HIP error.
+int ceil_read3_write(const float* a, const float* b, const float* c, int64_t n, int64_t entries,
+                     int64_t* out_idx, uint16_t* out_val, int32_t blocks_per_cu, uint32_t* sink,
+                     void* stream)
+{
+    if (!a || !b || !c || !sink || !out_idx || !out_val || n < 0 || entries < 0 ||
+        entries > ((int64_t)1 << 40) || blocks_per_cu <= 0 ||
+        ((reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b) |
+          reinterpret_cast<uintptr_t>(c)) & 15u) != 0 ||
+        (reinterpret_cast<uintptr_t>(out_idx) & 7u) != 0 ||
+        (reinterpret_cast<uintptr_t>(out_val) & 1u) != 0)
+        return 1;
+    const int64_t tiles = n / kTile;
+    if (tiles == 0) return 0;
+    if (entries > 0 && tiles > ((int64_t)1 << 62) / entries) return 1;   // E (t+1) fits int64
+    const dim3 grid((unsigned)(cus_of_current() * blocks_per_cu));
+    hipLaunchKernelGGL(read3_write_kernel, grid, dim3(kBlock), 0, (hipStream_t)stream, a, b, c,
+                       tiles, entries, out_idx, out_val, sink);
+    return hipGetLastError() == hipSuccess ? 0 : 4;
+}
+
+// The (offset, value) writes of ceil_read3_write alone: entries [0,
+// entries) of out_idx / out_val (device; out_idx 8-byte aligned), each wave
+// one contiguous range; blocks_per_cu blocks of 256 threads per CU.  The
+// written values are meaningless.  Returns 0, 1 on a bad argument, 4 on a
+// HIP error.
+int ceil_write_entries(int64_t entries, int64_t* out_idx, uint16_t* out_val,
+                       int32_t blocks_per_cu, void* stream)
+{
+    if (!out_idx || !out_val || entries < 0 || entries > ((int64_t)1 << 40) ||
+        blocks_per_cu <= 0 || (reinterpret_cast<uintptr_t>(out_idx) & 7u) != 0 ||
+        (reinterpret_cast<uintptr_t>(out_val) & 1u) != 0)
+        return 1;
+    if (entries == 0) return 0;
+    const dim3 grid((unsigned)(cus_of_current() * blocks_per_cu));
+    hipLaunchKernelGGL(write_entries_kernel, grid, dim3(kBlock), 0, (hipStream_t)stream, entries,
+                       out_idx, out_val);
     return hipGetLastError() == hipSuccess ? 0 : 4;
 }
 

@@ -5,7 +5,9 @@
 //
 // Design (HBM-bound: 12 bytes read per element, ~10 bytes written per
 // changed element):
-//  - persistent grid (3 blocks of 4 waves per CU); each wave owns one
+//  - persistent grid of one block of 12 waves per CU (three per SIMD, the
+//    VGPR limit; the block holds the CU's whole LDS) over the full tiles,
+//    three blocks of 4 waves per CU over ragged ones; each wave owns one
 //    contiguous range of 2048-element tiles, ranges ascending with the
 //    global wave number, so every wave's entries leave in ascending order;
 //    a wave loads eight float4 of p, m and v per lane, i.e. 24 16-byte
@@ -33,8 +35,8 @@
 //    atomicAdd on the 64-bit cursor per flush of its staging area, always
 //    exactly 1024 entries except a wave's last flush (so the output is made
 //    of whole 1024-entry runs, each ascending, until the waves finish), then
-//    writes the entries out coalesced.  No block-wide barrier anywhere; the number of
-//    atomics is bounded by entries / 1024 + waves;
+//    writes the entries out coalesced; in the unordered call the waves of a
+//    block combine their reservations (block_round below);
 //  - ordered mode: each flush also records (unordered position, entries of
 //    the wave before it, count, wave) and each wave its total; a scan of the
 //    wave totals and a copy of the recorded runs then give the entries in
@@ -50,13 +52,15 @@
 namespace dte {
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kWaves = kBlock / 64;
+// Waves per block: 12 (one block per CU) for full tiles; the ragged-tile
+// kernels need more VGPRs than 12 waves per CU leave without spilling, and
+// run as 4-wave blocks, three per CU.  Either way 3 waves per SIMD.
+template <bool kFull> constexpr int kWavesOf = kFull ? 12 : 4;
+constexpr int kWavesPerCU = 12;
 constexpr int kVec = 8;                       // float4 per lane per array per tile
 constexpr int kSlots = 4 * kVec;              // elements per lane per tile
 constexpr int kWaveTile = 64 * kSlots;        // 2048 elements per wave tile
 constexpr int kQueue = 256;                   // queued candidates per wave (16 bytes each)
-constexpr int kBlocksPerCU = 3;               // 3 waves per SIMD (VGPR-bound), 40 KB LDS
 // a float4 slot selects up to 4 x 64 elements at once: they must fit an
 // empty candidate queue, and the part left after one flush of the staging
 // area must fit the emptied area
@@ -391,7 +395,7 @@ __device__ __forceinline__ void stage_changed(const ExtractParams& a, const Wave
 }
 
 // Combined flushes of the unordered call.  Every kRound tiles, and once at
-// the end, the four waves of a block meet at a barrier; when they hold at
+// the end, the kW waves of a block meet at a barrier; when they hold at
 // least kBlockFlush staged entries (at the end: any), one atomicAdd on the
 // cursor reserves room for all of them and each wave writes its entries
 // after those of the waves before it.  Every wave of the device reserving
@@ -401,22 +405,23 @@ __device__ __forceinline__ void stage_changed(const ExtractParams& a, const Wave
 // own.  Block-uniform control flow; the two LDS slots alternate, so a slot
 // is rewritten only after every wave has passed a later barrier.
 constexpr int kRound = 4;
-constexpr int kBlockFlush = 3 * 1024;
+constexpr int kFlushPerWave = 768;            // block flush threshold per wave
 
+template <int kW>
 __device__ void block_round(const ExtractParams& a, const WaveStage& st, Staging& so, int lane,
-                            int wave, int (*s_cnt)[kWaves], unsigned long long* s_base, int slot,
+                            int wave, int (*s_cnt)[kW], unsigned long long* s_base, int slot,
                             bool last_round)
 {
     if (lane == 0) s_cnt[slot][wave] = so.staged;
     __syncthreads();
     int total = 0, before = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < kW; ++w) {
         const int c = s_cnt[slot][w];
         total += c;
         before += w < wave ? c : 0;
     }
-    if (total == 0 || (!last_round && total < kBlockFlush)) return;
+    if (total == 0 || (!last_round && total < kW * kFlushPerWave)) return;
     if (threadIdx.x == 0)
         s_base[slot] = atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor),
                                  (unsigned long long)total);
@@ -570,9 +575,10 @@ __device__ __forceinline__ void process_tile(const ExtractParams& a, int64_t t0,
 
 // Wave tiles [first, last) of the range; kFull: each lies inside [0, n).
 template <bool kFull, bool kVecLoads, bool kDecayOne, bool kWritePrev, bool kLit, bool kRoute>
-__global__ __launch_bounds__(kBlock) void extract_kernel(ExtractParams a, int64_t first,
-                                                         int64_t last)
+__global__ __launch_bounds__(64 * kWavesOf<kFull>) void extract_kernel(ExtractParams a,
+                                                                      int64_t first, int64_t last)
 {
+    constexpr int kWaves = kWavesOf<kFull>;
     __shared__ uint32_t s_key[kWaves][kWaveStage];
     __shared__ uint16_t s_val[kWaves][kWaveStage];
     __shared__ float s_qp[kWaves][kQueue];
@@ -664,14 +670,25 @@ __global__ __launch_bounds__(256) void adamw_forward_kernel(ForwardParams a)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Blocks that one launch over wave tiles [first, last) uses, at most
+// max_waves waves.
+template <bool F>
+int64_t blocks_of(int64_t first, int64_t last, int64_t max_waves)
+{
+    if (last <= first) return 0;
+    const int64_t b = (last - first + kWavesOf<F> - 1) / kWavesOf<F>;
+    const int64_t cap = max_waves / kWavesOf<F>;
+    return b < cap ? b : cap;
+}
+
 // Launch over wave tiles [first, last); returns the number of waves.
 template <bool F, bool V, bool D, bool L, bool R>
-int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_grid,
+int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_waves,
                      int32_t wave0, hipStream_t s)
 {
     if (last <= first) return 0;
-    const int64_t blocks = (last - first + kWaves - 1) / kWaves;
-    const dim3 grid((unsigned)(blocks < max_grid ? blocks : max_grid));
+    constexpr int kBlock = 64 * kWavesOf<F>;
+    const dim3 grid((unsigned)blocks_of<F>(first, last, max_waves));
     a.wave0 = wave0;
     if (R)   // routing mode: no theta_hat output
         hipLaunchKernelGGL((extract_kernel<F, V, D, false, L, R>), grid, dim3(kBlock), 0, s, a, first,
@@ -682,19 +699,19 @@ int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_g
     else
         hipLaunchKernelGGL((extract_kernel<F, V, D, false, L, false>), grid, dim3(kBlock), 0, s, a,
                            first, last);
-    return (int32_t)grid.x * kWaves;
+    return (int32_t)grid.x * kWavesOf<F>;
 }
 
 template <bool D, bool L, bool R>
-int32_t launch_all(const ExtractParams& a, bool vec, int64_t max_grid, hipStream_t s)
+int32_t launch_all(const ExtractParams& a, bool vec, int64_t max_waves, hipStream_t s)
 {
     const int64_t full = a.n / kWaveTile;
     const int64_t ntiles = (a.n + kWaveTile - 1) / kWaveTile;
     if (vec) {
-        const int32_t w = launch_tiles<true, true, D, L, R>(a, 0, full, max_grid, 0, s);  // unguarded
-        return w + launch_tiles<false, true, D, L, R>(a, full, ntiles, max_grid, w, s);   // ragged
+        const int32_t w = launch_tiles<true, true, D, L, R>(a, 0, full, max_waves, 0, s);  // unguarded
+        return w + launch_tiles<false, true, D, L, R>(a, full, ntiles, max_waves, w, s);   // ragged
     }
-    return launch_tiles<false, false, D, L, R>(a, 0, ntiles, max_grid, 0, s);           // scalar loads
+    return launch_tiles<false, false, D, L, R>(a, 0, ntiles, max_waves, 0, s);           // scalar loads
 }
 
 // ---- ordered mode: runs to ascending positions ----------------------------
@@ -731,6 +748,7 @@ __global__ __launch_bounds__(1024) void order_scan_kernel(OrderParams o)
     if (tid == 0) *o.cursor = c0 + part[kThreads - 1];
 }
 
+constexpr int kCopyBlock = 256;
 constexpr int kCopySlots = 8;                  // entries per lane per copy chunk
 constexpr int kCopyChunk = 64 * kCopySlots;
 
@@ -739,11 +757,11 @@ constexpr int kCopyChunk = 64 * kCopySlots;
 // + c kCopyChunk + i), all loads of a chunk before its stores.  Then whole
 // recorded runs: entry i of a run moves from src + i to wave_base[wave] +
 // woff + i.
-__global__ __launch_bounds__(kBlock) void order_copy_kernel(OrderParams o)
+__global__ __launch_bounds__(kCopyBlock) void order_copy_kernel(OrderParams o)
 {
     const int lane = threadIdx.x & 63;
-    const int64_t w = (int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6);
-    const int64_t nw = (int64_t)gridDim.x * kWaves;
+    const int64_t w = (int64_t)blockIdx.x * (kCopyBlock / 64) + (threadIdx.x >> 6);
+    const int64_t nw = (int64_t)gridDim.x * (kCopyBlock / 64);
     const int64_t per_region = (o.region_size + kCopyChunk - 1) / kCopyChunk;
     const int64_t chunks = (int64_t)o.waves * per_region;
     const int64_t* __restrict__ ridx = o.region_idx;
@@ -794,31 +812,31 @@ hipError_t launch_order(const OrderParams& o, int cus, hipStream_t stream)
 {
     if (o.waves <= 0) return hipSuccess;
     hipLaunchKernelGGL(order_scan_kernel, dim3(1), dim3(1024), 0, stream, o);
-    hipLaunchKernelGGL(order_copy_kernel, dim3((unsigned)cus * 8), dim3(kBlock), 0, stream, o);
+    hipLaunchKernelGGL(order_copy_kernel, dim3((unsigned)cus * 8), dim3(kCopyBlock), 0, stream, o);
     return hipGetLastError();
 }
 
 namespace {
 
 // Waves that launch_all launches (its grid rule).
-int64_t waves_of(int64_t n, bool vec, int64_t max_grid)
+int64_t waves_of(int64_t n, bool vec, int64_t max_waves)
 {
-    const auto blocks = [max_grid](int64_t first, int64_t last) -> int64_t {
-        if (last <= first) return 0;
-        const int64_t b = (last - first + kWaves - 1) / kWaves;
-        return b < max_grid ? b : max_grid;
-    };
     const int64_t full = n / kWaveTile;
     const int64_t ntiles = (n + kWaveTile - 1) / kWaveTile;
-    return (vec ? blocks(0, full) + blocks(full, ntiles) : blocks(0, ntiles)) * kWaves;
+    if (vec)
+        return blocks_of<true>(0, full, max_waves) * kWavesOf<true> +
+               blocks_of<false>(full, ntiles, max_waves) * kWavesOf<false>;
+    return blocks_of<false>(0, ntiles, max_waves) * kWavesOf<false>;
 }
 
-int64_t max_grid_of(const ExtractParams& a, int cus)
+// Waves per launch at most.  Ordered mode: both launches together stay
+// within kMaxOrderedWaves (the ragged launch covers one tile: one block).
+int64_t max_waves_of(const ExtractParams& a, int cus)
 {
-    int64_t max_grid = (int64_t)cus * kBlocksPerCU;
-    // ordered mode: both launches together stay within kMaxOrderedWaves
-    if (a.runs && max_grid > kMaxOrderedWaves / kWaves - 1) max_grid = kMaxOrderedWaves / kWaves - 1;
-    return max_grid;
+    int64_t max_waves = (int64_t)cus * kWavesPerCU;
+    const int64_t ordered_cap = kMaxOrderedWaves - kWavesOf<false>;
+    if (a.runs && max_waves > ordered_cap) max_waves = ordered_cap;
+    return max_waves;
 }
 
 bool vector_loads(const ExtractParams& a)
@@ -831,30 +849,30 @@ bool vector_loads(const ExtractParams& a)
 
 int64_t extract_waves(const ExtractParams& a, int cus)
 {
-    return a.n > 0 ? waves_of(a.n, vector_loads(a), max_grid_of(a, cus)) : 0;
+    return a.n > 0 ? waves_of(a.n, vector_loads(a), max_waves_of(a, cus)) : 0;
 }
 
 hipError_t launch_extract(const ExtractParams& a, int cus, hipStream_t stream, int32_t* waves)
 {
     if (waves) *waves = 0;
     if (a.n <= 0) return hipSuccess;
-    const int64_t max_grid = max_grid_of(a, cus);
+    const int64_t max_waves = max_waves_of(a, cus);
     const bool vec = vector_loads(a);
     int32_t w;
     const bool one = a.decay == 1.0f;
     if (a.route) {
         if (a.literal)
-            w = one ? launch_all<true, true, true>(a, vec, max_grid, stream)
-                    : launch_all<false, true, true>(a, vec, max_grid, stream);
+            w = one ? launch_all<true, true, true>(a, vec, max_waves, stream)
+                    : launch_all<false, true, true>(a, vec, max_waves, stream);
         else
-            w = one ? launch_all<true, false, true>(a, vec, max_grid, stream)
-                    : launch_all<false, false, true>(a, vec, max_grid, stream);
+            w = one ? launch_all<true, false, true>(a, vec, max_waves, stream)
+                    : launch_all<false, false, true>(a, vec, max_waves, stream);
     } else if (a.literal) {
-        w = one ? launch_all<true, true, false>(a, vec, max_grid, stream)
-                : launch_all<false, true, false>(a, vec, max_grid, stream);
+        w = one ? launch_all<true, true, false>(a, vec, max_waves, stream)
+                : launch_all<false, true, false>(a, vec, max_waves, stream);
     } else {
-        w = one ? launch_all<true, false, false>(a, vec, max_grid, stream)
-                : launch_all<false, false, false>(a, vec, max_grid, stream);
+        w = one ? launch_all<true, false, false>(a, vec, max_waves, stream)
+                : launch_all<false, false, false>(a, vec, max_waves, stream);
     }
     if (waves) *waves = w;
     return hipGetLastError();

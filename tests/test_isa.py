@@ -7,8 +7,8 @@ this repository's own sources, gfx950):
   write-back or discard): outputs go through vector stores only;
 * no scratch memory (no register spills) in any kernel;
 * the hot extract kernels (full tiles, vector loads, no theta_hat output)
-  fit three waves per SIMD and three blocks per CU: at most 168 VGPRs and a
-  third of the CU's 160 KB of LDS per block.
+  fit three waves per SIMD as one 12-wave block per CU: at most 168 VGPRs
+  and the CU's 160 KB of LDS per block.
 """
 import os
 import re
@@ -95,6 +95,6 @@ def test_hot_extract_kernels_fit_three_waves_per_simd(assembly):
             hot.append(name)
             assert int(f["vgpr_count"]) <= 168, (name, f["vgpr_count"])
             assert int(f["agpr_count"]) == 0, name
-            assert int(f["group_segment_fixed_size"]) <= 160 * 1024 // 3, name
+            assert int(f["group_segment_fixed_size"]) <= 160 * 1024, name
     # decay == 1 or not, folded or literal order, with or without routing
     assert len(hot) == 8

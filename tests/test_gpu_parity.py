@@ -600,3 +600,56 @@ def test_dense_delta_spanning_many_rounds(lr):
         pipe.close()
     del p, m, v
     torch.cuda.empty_cache()
+
+
+def straddling_state(sc, n, seed):
+    """Weights just below a BF16 rounding midpoint (above one, for negative
+    weights) and step terms that carry the reconstruction to within about
+    2^-21 relatively of that midpoint, on both sides of it: the elements
+    whose change only the exact inverse can settle, mixed with ones an
+    approximate bound settles."""
+    rng = np.random.default_rng(seed)
+    hi = (rng.integers(0x3A00, 0x4000, n, dtype=np.uint32) & 0x7FFF)    # |p| ~ 5e-4 .. 2
+    mid = ((hi << 16) | 0x8000).view(np.float32).astype(np.float64)     # midpoint above hi
+    gap = np.ldexp(mid, -rng.integers(9, 22, n))                       # 2^-9 .. 2^-21 below it
+    p = (mid - gap).astype(np.float32)
+    decay = float(sc.decay)
+    # theta_hat = (p + u) / decay lands on the midpoint for u = mid decay - p
+    target = mid * decay - p.astype(np.float64)
+    target *= 1.0 + rng.integers(-48, 49, n) * 2.0 ** -21
+    v = (10.0 ** rng.uniform(-12, -4, n)).astype(np.float32)
+    den = np.sqrt(v.astype(np.float64) * float(sc.rbc2)) + float(sc.eps)
+    m = (target * den / float(sc.lrb1)).astype(np.float32)
+    neg = rng.random(n) < 0.5                                          # mirror half of them
+    p[neg] = -p[neg]
+    m[neg] = -m[neg]
+    return p, m, v
+
+
+@pytest.mark.parametrize("lr", [1e-6, 1e-4, 3e-2])
+@pytest.mark.parametrize("order", [W.ORDER_FOLDED, W.ORDER_LITERAL])
+def test_step_terms_straddling_the_bf16_midpoint(lr, order):
+    """Reconstructions within a few binary32 ulps of a BF16 rounding
+    midpoint, on either side: every element parity-checked against the
+    oracle, with and without theta_hat requested."""
+    say("case: straddling midpoints", lr, order)
+    n = (1 << 18) + 77
+    hp = W.StepHP(lr=lr, order=order)
+    sc = ocore.derive_scalars(hp)
+    p, m, v = straddling_state(sc, n, 29)
+    want_idx, want_val, want_ph = ocore.detect(p, m, v, sc, 0)
+    # the inputs do straddle: both outcomes are common
+    assert 0.2 * n < want_idx.size < 0.8 * n, want_idx.size
+    spec = layouts.build_spec(W.scaled_dense(layers=1, tp=2))
+    pipe = DeltaPipeline(spec, capacity=n)
+    for with_prev in (False, True):
+        prev = torch.empty(n, dtype=torch.float32, device="cuda") if with_prev else None
+        pipe.reset()
+        pipe.extract(dev(p), dev(m), dev(v), hp, out_prev=prev)
+        sync()
+        idx, val, total = pipe.delta()
+        assert total == want_idx.size, with_prev
+        assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val), with_prev
+        if with_prev:
+            assert np.array_equal(prev.cpu().numpy().view(np.uint32), want_ph.view(np.uint32))
+    pipe.close()

@@ -46,8 +46,10 @@ def test_traffic_record_lookup(path):
     total = (sum(rec["fetch_size_kib_per_call"].values()) * 1024 * cal["fetch_factor"] +
              sum(rec["write_size_kib_per_call"].values()) * 1024 * cal["write_factor"])
     assert abs(total - got) < 1.0
-    # within a fraction of a percent of extract's algorithmic bytes 12 N + 10 M
-    assert 1.0 <= got / rec["algorithmic_bytes_per_launch"] < 1.01
+    # within about one percent of extract's algorithmic bytes 12 N + 10 M
+    # (the dense sweep point writes partial lines at the ends of its runs:
+    # its WRITE_SIZE is about 1.1 x its 10 M bytes)
+    assert 1.0 <= got / rec["algorithmic_bytes_per_launch"] < 1.02
 
 
 def test_traffic_is_withheld_for_another_mode_or_workload():

@@ -57,8 +57,9 @@ class WindowResult:
     p_prev: Optional[np.ndarray] = None
 
 
-def state(wl, k: int, lo: int, hi: int, sc: core.Scalars, threads: int = 1):
-    """Pre-step draws and the post-step state of tensor k, elements [lo, hi)."""
+def draws(wl, k: int, lo: int, hi: int, threads: int = 1):
+    """Pre-step weights, moments and gradient of tensor k, elements [lo, hi)
+    (zero moments and gradient for an untouched tensor)."""
     t = wl.tensors[k]
     n = hi - lo
     p_prev = synth.draw_cpu(n, wl.seed, k, KIND_P_PREV, lo, threads)
@@ -70,6 +71,12 @@ def state(wl, k: int, lo: int, hi: int, sc: core.Scalars, threads: int = 1):
         m_prev = np.zeros(n, np.float32)
         v_prev = np.zeros(n, np.float32)
         g = np.zeros(n, np.float32)
+    return p_prev, m_prev, v_prev, g
+
+
+def state(wl, k: int, lo: int, hi: int, sc: core.Scalars, threads: int = 1):
+    """Pre-step draws and the post-step state of tensor k, elements [lo, hi)."""
+    p_prev, m_prev, v_prev, g = draws(wl, k, lo, hi, threads)
     p, m, v = core.adamw_forward(p_prev, m_prev, v_prev, g, sc)
     return p_prev, p, m, v
 

@@ -653,3 +653,36 @@ def test_step_terms_straddling_the_bf16_midpoint(lr, order):
         if with_prev:
             assert np.array_equal(prev.cpu().numpy().view(np.uint32), want_ph.view(np.uint32))
     pipe.close()
+
+
+@pytest.mark.parametrize("order", [W.ORDER_FOLDED, W.ORDER_LITERAL])
+def test_extract_on_torch_adamw_states(order):
+    """The tiny block stepped by torch.optim.AdamW (another trainer's
+    rounding of the same step): delta and theta_hat equal the oracle's on
+    that state."""
+    from oracle import mode_b
+    from oracle import run as orun_
+    say("case: torch-stepped state", order)
+    wl = W.tiny_block()
+    hp = W.StepHP(lr=wl.hp.lr, order=order, weight_decay=wl.hp.weight_decay, step=wl.hp.step)
+    parts = [mode_b.torch_adamw_step(*orun_.draws(wl, k, 0, t.numel), hp)
+             for k, t in enumerate(wl.tensors)]
+    p, m, v = (np.concatenate([x[i] for x in parts]) for i in range(3))
+    want_idx, want_val, want_ph = ocore.detect(p, m, v, ocore.derive_scalars(hp), 0)
+    assert want_idx.size > 1000
+    spec = layouts.build_spec(wl)
+    pipe = DeltaPipeline(spec, capacity=p.size)
+    prev = torch.empty(p.size, dtype=torch.float32, device="cuda")
+    pipe.reset()
+    pipe.extract(dev(p), dev(m), dev(v), hp, out_prev=prev)
+    sync()
+    idx, val, total = pipe.delta()
+    assert total == want_idx.size
+    assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val)
+    assert np.array_equal(prev.cpu().numpy().view(np.uint32), want_ph.view(np.uint32))
+    pipe.reset()
+    pipe.extract(dev(p), dev(m), dev(v), hp)
+    sync()
+    idx, val, total = pipe.delta()
+    assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val)
+    pipe.close()

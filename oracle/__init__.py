@@ -17,6 +17,9 @@ Modules, each following the paper's passage named in its header:
   mcore  -- Megatron-Core sender layout and converter (appendix B,
             eq. mcore_fused_qkv, eq. mcore_tp_shard, eq. qkv_converter):
             detection in the paper's order for one trainer TP rank
+  timing, recipe_compare, mode_b -- reports built on the above: the CPU
+            baseline's timing, the input recipe's effect, and the
+            reconstruction counts when torch.optim.AdamW takes the step
 
 Pins (tests/test_oracle_*.py) tie every function to the paper and to
 mathematics outside this package.  Parity unpinned: the change fraction and

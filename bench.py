@@ -97,7 +97,7 @@ def measured_traffic(workload_name, kernel, mode):
     return rec["traffic_bytes_per_launch"]
 
 
-def ceilings(p, m, v, pipe, stream, entries, reps=5):
+def ceilings(p, m, v, pipe, stream, entries, reps=5, touch=None):
     """Second denominators measured on the same GPU and buffers: the rate of
     a plain read of theta, m, v (12 bytes per element, extract's access
     pattern, no arithmetic, no stores; best of 2, 3 and 4 blocks per CU);
@@ -108,7 +108,8 @@ def ceilings(p, m, v, pipe, stream, entries, reps=5):
     same writes issued together with the read (a naive mix); and the time of
     writing whole 64-byte lines at every apply address of the step's
     buckets (into scratch buffers of the shards' size; best of 4, 8 and 16
-    blocks per CU)."""
+    blocks per CU).  touch: run before every repetition, outside its
+    events (the cache flush of a state that fits the last-level cache)."""
     import ctypes
 
     import torch
@@ -132,6 +133,8 @@ def ceilings(p, m, v, pipe, stream, entries, reps=5):
     def timed(fn, name):
         best = None
         for _ in range(reps + 1):                       # the first is a warm-up
+            if touch is not None:
+                touch()
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
             rc = fn()
@@ -464,12 +467,10 @@ def main():
     if not apply_only:
         out["config"].update({"extract_ms": ext["mean"], "remap_ms": rem["mean"],
                               "apply_ms": app["mean"]})
-    if flush is not None:
-        del flush
-        torch.cuda.empty_cache()
     if not args.no_ceilings:
         log("bench: reference read stream and scattered lines")
-        ce = ceilings(p, m, v, pipe, stream, 0 if apply_only else changed)
+        ce = ceilings(p, m, v, pipe, stream, 0 if apply_only else changed,
+                      touch=(lambda: flush.add_(1.0)) if flush is not None else None)
         rs = ce["read_stream"]
         if kernel == "extract":
             rs["kernel_frac"] = achieved / rs["gbs"]
@@ -480,6 +481,9 @@ def main():
             ce["apply_scattered_lines"]["apply_frac"] = \
                 ce["apply_scattered_lines"]["ms"] / app["mean"]
         out["roofline"]["ceilings"] = ce
+    if flush is not None:
+        del flush
+        torch.cuda.empty_cache()
     if args.store and not apply_only:
         out["storage"] = storage_leg(args.store, wl, spec, p, m, v, hp, cap)
     del p, m, v

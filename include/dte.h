@@ -124,11 +124,13 @@ dte_status dte_derive_scalars(const dte_adamw_step* hp, dte_scalars* out);
  *           several groups = several calls on their sub-ranges).
  * out_idx : device int64[capacity]; out_val: device uint16[capacity].
  * cursor  : device int64, append semantics: on entry the fill level of
- *           out_idx/out_val (0 for a fresh delta), on completion the total
- *           number of entries including those that did not fit.  Entries at
- *           positions >= capacity are dropped; after a stream
+ *           out_idx/out_val (0 for a fresh delta, below 2^36), on completion
+ *           the total number of entries including those that did not fit.
+ *           Entries at positions >= capacity are dropped; after a stream
  *           synchronisation, *cursor > capacity means the delta is
  *           incomplete and must be recomputed with capacity >= *cursor.
+ *           While the call runs, its bits from 36 up count the work units
+ *           that blocks take (cleared by the call's last kernel).
  * out_prev: device binary32[n] receiving theta_hat, or NULL (no write).
  * Entry order is unspecified (the set of entries is exact; each wave of the
  * kernel writes its entries in ascending runs); offsets are unique within

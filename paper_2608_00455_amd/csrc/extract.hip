@@ -10,6 +10,10 @@
 //    three blocks of 4 waves per CU over ragged ones; each wave owns one
 //    contiguous range of 2048-element tiles, ranges ascending with the
 //    global wave number, so every wave's entries leave in ascending order;
+//    in the unordered call the static ranges leave out the last 1/16 of
+//    the full tiles, which blocks then take four tiles per wave at a time
+//    from a counter (the CUs do not stream at one rate, and a static split
+//    leaves the fast ones idle at the end);
 //    a wave loads eight float4 of p, m and v per lane, i.e. 24 16-byte
 //    non-temporal loads in flight per lane, which is what keeps the HBM
 //    queues full at this occupancy;
@@ -175,6 +179,24 @@ __device__ __forceinline__ float exact_prev(float p, float m, float v, const Ext
 constexpr int kTileBits = __builtin_ctz(kWaveTile);
 constexpr int64_t kDenseRatio = 64;             // see flush_wave
 static_assert((1 << kTileBits) == kWaveTile, "wave tile must be a power of two");
+
+// Dynamic tail of the unordered call over full tiles: the last
+// total / kTailDiv tiles (at most 2^20, so that a tile's offset from the
+// tail's start fits a staging key) go to blocks four tiles per wave (one
+// flush round) per grab.  A grab adds 2^kGrabShift to the caller's cursor, whose bits below
+// kGrabShift count the entries (a delta never reaches 2^36 entries): the
+// old value's high bits number the chunk, every reservation masks them off,
+// and clear_grabs_kernel clears them once the kernel is done.
+constexpr int64_t kTailDiv = 16;
+constexpr int64_t kMaxTailTiles = (int64_t)1 << 20;
+constexpr int kGrabShift = 36;
+constexpr unsigned long long kCountMask = (1ull << kGrabShift) - 1;
+
+__host__ __device__ inline int64_t tail_tiles(int64_t tiles, bool dynamic)
+{
+    const int64_t d = dynamic ? tiles / kTailDiv : 0;
+    return d < kMaxTailTiles ? d : kMaxTailTiles;
+}
 // Per-wave LDS areas.  Keys are (wave iteration << kTileBits) | element in
 // the tile; the wave's tiles are t_first + iteration.
 struct WaveStage {
@@ -315,7 +337,7 @@ __device__ void flush_wave(const ExtractParams& a, const WaveStage& st, Staging&
     unsigned long long base = 0;
     if (lane == 0) {
         base = atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor),
-                         (unsigned long long)staged);
+                         (unsigned long long)staged) & kCountMask;
         if (a.runs) {
             const unsigned long long r =
                 atomicAdd(reinterpret_cast<unsigned long long*>(a.run_cursor), 1ull);
@@ -424,7 +446,7 @@ __device__ void block_round(const ExtractParams& a, const WaveStage& st, Staging
     if (total == 0 || (!last_round && total < kW * kFlushPerWave)) return;
     if (threadIdx.x == 0)
         s_base[slot] = atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor),
-                                 (unsigned long long)total);
+                                 (unsigned long long)total) & kCountMask;
     __syncthreads();
     if (so.staged > 0) write_staged(a, st, so, (int64_t)s_base[slot] + before, lane);
 }
@@ -587,22 +609,28 @@ __global__ __launch_bounds__(64 * kWavesOf<kFull>) void extract_kernel(ExtractPa
     __shared__ uint32_t s_qkey[kWaves][kQueue];
     __shared__ int s_cnt[2][kWaves];
     __shared__ unsigned long long s_base[2];
+    __shared__ int64_t s_chunk;
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    // wave g of the launch owns the contiguous tile range [g per, (g+1) per)
     const int64_t g = (int64_t)blockIdx.x * kWaves + wave;
     const int64_t nw = (int64_t)gridDim.x * kWaves;
-    const int64_t per = (last - first + nw - 1) / nw;
+    // unordered output: combined flushes (block_round); every wave of the
+    // block runs the same iterations, so the barriers match
+    const bool combine = !kRoute && a.runs == nullptr;
+    // wave g owns the contiguous tile range [g per, (g+1) per) of the
+    // static part [first, s_last); the tail [s_last, last) is dynamic
+    constexpr bool kTail = kFull && !kRoute;     // a dynamic tail is possible
+    const int64_t tail = kTail ? tail_tiles(last - first, combine) : 0;
+    const int64_t s_last = last - tail;
+    const int64_t per = (s_last - first + nw - 1) / nw;
     const int64_t w_first = first + g * per;
-    const int64_t w_last = (w_first + per < last) ? w_first + per : last;
+    const int64_t w_last = (w_first + per < s_last) ? w_first + per : s_last;
     Staging so{0, 0, 0, 0};
     const WaveStage st{s_key[wave], s_val[wave], s_qp[wave], s_qm[wave], s_qv[wave],
                        s_qkey[wave], w_first, a.wave0 + (int32_t)g};
-    // unordered output: combined flushes (block_round); every wave of the
-    // block runs the same `per` iterations, so the barriers match
-    const bool combine = !kRoute && a.runs == nullptr;
     int queued = 0;
+    int round = 0;                               // block_round calls so far (LDS slot parity)
     for (int64_t it = 0; it < per; ++it) {
         const int64_t t = w_first + it;
         if (t < w_last) {
@@ -612,13 +640,42 @@ __global__ __launch_bounds__(64 * kWavesOf<kFull>) void extract_kernel(ExtractPa
                 a, t * kWaveTile, lane, so, queued, st, (uint32_t)it, P, M, V);
         }
         if (combine && it % kRound == kRound - 1)
-            block_round(a, st, so, lane, wave, s_cnt, s_base, (int)((it / kRound) & 1), false);
+            block_round(a, st, so, lane, wave, s_cnt, s_base, (round++) & 1, false);
     }
     if (queued > 0) drain_queue<kDecayOne, kLit, kRoute>(a, st, queued, so, lane);
-    if (combine)
-        block_round(a, st, so, lane, wave, s_cnt, s_base, (int)((per / kRound) & 1), true);
-    else if (so.staged > 0)
+    if (kTail && tail > 0) {
+        // staged keys count tiles from the stage's first tile: empty the
+        // staging areas, then count from the tail's start
+        block_round(a, st, so, lane, wave, s_cnt, s_base, (round++) & 1, true);
+        const WaveStage tst{s_key[wave], s_val[wave], s_qp[wave], s_qm[wave], s_qv[wave],
+                            s_qkey[wave], s_last, st.wave};
+        for (;;) {
+            if (threadIdx.x == 0)
+                s_chunk = (int64_t)(atomicAdd(reinterpret_cast<unsigned long long*>(a.cursor),
+                                              1ull << kGrabShift) >> kGrabShift);
+            __syncthreads();
+            const int64_t c = s_chunk * (kWaves * kRound);   // block-uniform
+            __syncthreads();                                 // s_chunk is rewritten next
+            if (c >= tail) break;
+            for (int i = 0; i < kRound; ++i) {
+                const int64_t rel = c + (int64_t)wave * kRound + i;   // tile s_last + rel
+                if (rel < tail) {
+                    f32x4 P[kVec], M[kVec], V[kVec];
+                    load_tile<kFull, kVecLoads>(a, (s_last + rel) * kWaveTile, lane, P, M, V);
+                    process_tile<kFull, kVecLoads, kDecayOne, kWritePrev, kLit, kRoute>(
+                        a, (s_last + rel) * kWaveTile, lane, so, queued, tst, (uint32_t)rel, P,
+                        M, V);
+                }
+            }
+            block_round(a, tst, so, lane, wave, s_cnt, s_base, (round++) & 1, false);
+        }
+        if (queued > 0) drain_queue<kDecayOne, kLit, kRoute>(a, tst, queued, so, lane);
+        block_round(a, tst, so, lane, wave, s_cnt, s_base, (round++) & 1, true);
+    } else if (combine) {
+        block_round(a, st, so, lane, wave, s_cnt, s_base, (round++) & 1, true);
+    } else if (so.staged > 0) {
         flush_wave<kRoute>(a, st, so, lane);
+    }
     if (a.runs && lane == 0) {
         a.wave_count[st.wave] = so.flushed;
         a.region_count[st.wave] = so.in_region;
@@ -668,6 +725,14 @@ __global__ __launch_bounds__(256) void adamw_forward_kernel(ForwardParams a)
     }
 }
 
+// After an unordered launch with a dynamic tail: the grab count leaves the
+// cursor's high bits (single thread; runs after the extract kernel on the
+// same stream).
+__global__ void clear_grabs_kernel(int64_t* cursor)
+{
+    *cursor = (int64_t)((unsigned long long)*cursor & kCountMask);
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Blocks that one launch over wave tiles [first, last) uses, at most
@@ -699,6 +764,8 @@ int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_w
     else
         hipLaunchKernelGGL((extract_kernel<F, V, D, false, L, false>), grid, dim3(kBlock), 0, s, a,
                            first, last);
+    if (F && !R && a.runs == nullptr && tail_tiles(last - first, true) > 0)
+        hipLaunchKernelGGL(clear_grabs_kernel, dim3(1), dim3(1), 0, s, a.cursor);
     return (int32_t)grid.x * kWavesOf<F>;
 }
 

@@ -686,3 +686,37 @@ def test_extract_on_torch_adamw_states(order):
     idx, val, total = pipe.delta()
     assert np.array_equal(idx, want_idx) and np.array_equal(val, want_val)
     pipe.close()
+
+
+@pytest.mark.parametrize("tiles", [15, 16, 1000, 20000])
+def test_unordered_tail_taken_in_chunks(tiles):
+    """The unordered call's last full tiles (1/16 of them) are taken by
+    blocks from a counter in the cursor's high bits: with a partial last
+    chunk, a tail too short to exist, and a cursor that already holds
+    entries (append), the delta equals the oracle's and the cursor ends at
+    the exact total."""
+    say("case: dynamic tail", tiles)
+    n = tiles * 2048 + 77
+    rng = np.random.default_rng(tiles)
+    p = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    m = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    v = np.abs(rng.standard_normal(n) * 1e-6).astype(np.float32)
+    hp = W.StepHP(lr=1e-4)
+    want_idx, want_val, _ = ocore.detect(p, m, v, ocore.derive_scalars(hp), 100)
+    assert want_idx.size > 0
+    cap = want_idx.size + 16
+    idx = torch.full((cap,), -1, dtype=torch.int64, device="cuda")
+    val = torch.zeros(cap, dtype=torch.int16, device="cuda")
+    cursor = torch.tensor([5], dtype=torch.int64, device="cuda")
+    dp, dm, dv = dev(p), dev(m), dev(v)
+    B.dte_extract_delta(dp.data_ptr(), dm.data_ptr(), dv.data_ptr(), n, 100, hp,
+                        idx.data_ptr(), val.data_ptr(), cap, cursor.data_ptr(), 0,
+                        torch.cuda.current_stream().cuda_stream)
+    sync()
+    assert int(cursor.item()) == 5 + want_idx.size
+    got_i = idx.cpu().numpy()
+    assert (got_i[:5] == -1).all()                         # entries before the cursor kept
+    got_v = val.cpu().numpy().view(np.uint16)[5:5 + want_idx.size]
+    got_i = got_i[5:5 + want_idx.size]
+    order = np.argsort(got_i)
+    assert np.array_equal(got_i[order], want_idx) and np.array_equal(got_v[order], want_val)

@@ -180,10 +180,10 @@ constexpr int kTileBits = __builtin_ctz(kWaveTile);
 constexpr int64_t kDenseRatio = 64;             // see flush_wave
 static_assert((1 << kTileBits) == kWaveTile, "wave tile must be a power of two");
 
-// Dynamic tail of the unordered call over full tiles: the last
-// total / kTailDiv tiles (at most 2^20, so that a tile's offset from the
-// tail's start fits a staging key) go to blocks four tiles per wave (one
-// flush round) per grab.  A grab adds 2^kGrabShift to the caller's cursor, whose bits below
+// Dynamic tail of the unordered call over full tiles: when the waves have
+// at least kTailDiv tiles each, the last total / kTailDiv tiles (at most
+// 2^20, so that a tile's offset from the tail's start fits a staging key)
+// go to blocks four tiles per wave (one flush round) per grab.  A grab adds 2^kGrabShift to the caller's cursor, whose bits below
 // kGrabShift count the entries (a delta never reaches 2^36 entries): the
 // old value's high bits number the chunk, every reservation masks them off,
 // and clear_grabs_kernel clears them once the kernel is done.
@@ -192,9 +192,9 @@ constexpr int64_t kMaxTailTiles = (int64_t)1 << 20;
 constexpr int kGrabShift = 36;
 constexpr unsigned long long kCountMask = (1ull << kGrabShift) - 1;
 
-__host__ __device__ inline int64_t tail_tiles(int64_t tiles, bool dynamic)
+__host__ __device__ inline int64_t tail_tiles(int64_t tiles, int64_t waves, bool dynamic)
 {
-    const int64_t d = dynamic ? tiles / kTailDiv : 0;
+    const int64_t d = dynamic && tiles >= kTailDiv * waves ? tiles / kTailDiv : 0;
     return d < kMaxTailTiles ? d : kMaxTailTiles;
 }
 // Per-wave LDS areas.  Keys are (wave iteration << kTileBits) | element in
@@ -621,7 +621,7 @@ __global__ __launch_bounds__(64 * kWavesOf<kFull>) void extract_kernel(ExtractPa
     // wave g owns the contiguous tile range [g per, (g+1) per) of the
     // static part [first, s_last); the tail [s_last, last) is dynamic
     constexpr bool kTail = kFull && !kRoute;     // a dynamic tail is possible
-    const int64_t tail = kTail ? tail_tiles(last - first, combine) : 0;
+    const int64_t tail = kTail ? tail_tiles(last - first, nw, combine) : 0;
     const int64_t s_last = last - tail;
     const int64_t per = (s_last - first + nw - 1) / nw;
     const int64_t w_first = first + g * per;
@@ -764,7 +764,8 @@ int32_t launch_tiles(ExtractParams a, int64_t first, int64_t last, int64_t max_w
     else
         hipLaunchKernelGGL((extract_kernel<F, V, D, false, L, false>), grid, dim3(kBlock), 0, s, a,
                            first, last);
-    if (F && !R && a.runs == nullptr && tail_tiles(last - first, true) > 0)
+    if (F && !R && a.runs == nullptr &&
+        tail_tiles(last - first, (int64_t)grid.x * kWavesOf<F>, true) > 0)
         hipLaunchKernelGGL(clear_grabs_kernel, dim3(1), dim3(1), 0, s, a.cursor);
     return (int32_t)grid.x * kWavesOf<F>;
 }

@@ -688,14 +688,18 @@ def test_extract_on_torch_adamw_states(order):
     pipe.close()
 
 
-@pytest.mark.parametrize("tiles", [15, 16, 1000, 20000])
-def test_unordered_tail_taken_in_chunks(tiles):
-    """The unordered call's last full tiles (1/16 of them) are taken by
-    blocks from a counter in the cursor's high bits: with a partial last
-    chunk, a tail too short to exist, and a cursor that already holds
+@pytest.mark.parametrize("case", ["small", "below", "exact", "partial"])
+def test_unordered_tail_taken_in_chunks(case):
+    """The unordered call's last full tiles (1/16 of them, once the waves
+    have 16 tiles each) are taken by blocks from a counter in the cursor's
+    high bits: just below that size (no tail), at it (whole chunks), above
+    it with a partial last chunk, and with a cursor that already holds
     entries (append), the delta equals the oracle's and the cursor ends at
     the exact total."""
-    say("case: dynamic tail", tiles)
+    waves = 12 * torch.cuda.get_device_properties(0).multi_processor_count
+    tiles = {"small": 15, "below": 16 * waves - 1, "exact": 16 * waves,
+             "partial": 16 * waves + 1000}[case]
+    say("case: dynamic tail", case, tiles)
     n = tiles * 2048 + 77
     rng = np.random.default_rng(tiles)
     p = (rng.standard_normal(n) * 0.02).astype(np.float32)

@@ -100,7 +100,9 @@ def measured_traffic(workload_name, kernel, mode):
 def ceilings(p, m, v, pipe, stream, entries, reps=5, touch=None):
     """Second denominators measured on the same GPU and buffers: the rate of
     a plain read of theta, m, v (12 bytes per element, extract's access
-    pattern, no arithmetic, no stores; best of 2, 3 and 4 blocks per CU);
+    pattern, no arithmetic, no stores; best of 2, 3 and 4 blocks per CU
+    with a static split and of one 12-wave block per CU taking four tiles
+    per wave at a time);
     the writes of an `entries`-entry delta alone (8-byte offsets and 2-byte
     values spread evenly over the tiles, into the pipeline's delta buffers,
     which the step has finished with; same block counts), whose time added
@@ -122,6 +124,8 @@ def ceilings(p, m, v, pipe, stream, entries, reps=5, touch=None):
     lib.ceil_read3_waves.argtypes = [I32]
     lib.ceil_read3.restype = ctypes.c_int
     lib.ceil_read3.argtypes = [P, P, P, I64, I32, P, P]
+    lib.ceil_read3_dynamic.restype = ctypes.c_int
+    lib.ceil_read3_dynamic.argtypes = [P, P, P, I64, P, P, P]
     lib.ceil_read3_write.restype = ctypes.c_int
     lib.ceil_read3_write.argtypes = [P, P, P, I64, I64, P, P, I32, P, P]
     lib.ceil_write_entries.restype = ctypes.c_int
@@ -156,6 +160,17 @@ def ceilings(p, m, v, pipe, stream, entries, reps=5, touch=None):
         if best is None or ms < best[0]:
             best = (ms, bpc)
         del sink
+    sink = torch.zeros(64 * lib.ceil_read3_waves(3), dtype=torch.int32, device="cuda")
+    counter = torch.zeros(1, dtype=torch.int64, device="cuda")
+
+    def dynamic_read():
+        counter.zero_()
+        return lib.ceil_read3_dynamic(p.data_ptr(), m.data_ptr(), v.data_ptr(), n,
+                                      counter.data_ptr(), sink.data_ptr(), s)
+    ms = timed(dynamic_read, "ceil_read3_dynamic")
+    if ms < best[0]:
+        best = (ms, "12-wave block, dynamic split")
+    del sink, counter
     out["read_stream"] = {"gbs": 12 * n / (best[0] / 1e3) / 1e9, "ms": best[0],
                           "blocks_per_cu": best[1], "bytes": 12 * n}
     e = min(entries, pipe.capacity)

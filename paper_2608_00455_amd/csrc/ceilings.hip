@@ -8,6 +8,9 @@
 //    (persistent grid, each wave a contiguous range of 2048-element tiles,
 //    eight 16-byte non-temporal loads per lane and array in flight) with no
 //    arithmetic beyond folding the loaded bits, and no stores;
+//    ceil_read3_dynamic: the same read by one 12-wave block per CU taking
+//    four tiles per wave at a time from a counter (the CUs do not stream at
+//    one rate, so a static split ends unevenly);
 //  - ceil_read3_write: the same read, plus the output extraction writes
 //    for a delta of a given size: 8-byte offsets (non-temporal stores) and
 //    2-byte values, spread evenly over the tiles, each wave writing its
@@ -65,6 +68,48 @@ __global__ __launch_bounds__(kBlock) void read3_kernel(const float* __restrict__
     }
     // a store the compiler cannot rule out keeps the loads; it practically
     // never happens
+    if (acc == 0x9E3779B9u) sink[g * 64 + lane] = acc;
+}
+
+// read3_kernel's read with blocks of 12 waves taking 4 tiles per wave at a
+// time: chunk k (from the counter) is tiles [48 k, 48 k + 48).
+constexpr int kDynWaves = 12;
+constexpr int kDynTiles = 4;
+
+__global__ __launch_bounds__(64 * kDynWaves) void read3_dynamic_kernel(
+    const float* __restrict__ a, const float* __restrict__ b, const float* __restrict__ c,
+    int64_t tiles, unsigned long long* __restrict__ counter, uint32_t* __restrict__ sink)
+{
+    __shared__ int64_t s_chunk;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    uint32_t acc = 0;
+    for (;;) {
+        if (threadIdx.x == 0) s_chunk = (int64_t)atomicAdd(counter, 1ull);
+        __syncthreads();
+        const int64_t c0 = s_chunk * (kDynWaves * kDynTiles);   // block-uniform
+        __syncthreads();                                        // s_chunk is rewritten next
+        if (c0 >= tiles) break;
+        for (int i = 0; i < kDynTiles; ++i) {
+            const int64_t t = c0 + (int64_t)wave * kDynTiles + i;
+            if (t >= tiles) break;
+            f32x4 A[kVec], B[kVec], C[kVec];
+#pragma unroll
+            for (int j = 0; j < kVec; ++j) {
+                const int64_t e = t * kTile + (int64_t)(j * 64 + lane) * 4;
+                A[j] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a + e));
+                B[j] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(b + e));
+                C[j] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(c + e));
+            }
+#pragma unroll
+            for (int j = 0; j < kVec; ++j) {
+                const u32x4 x = __builtin_bit_cast(u32x4, A[j]) ^ __builtin_bit_cast(u32x4, B[j]) ^
+                                __builtin_bit_cast(u32x4, C[j]);
+                acc ^= x.x ^ x.y ^ x.z ^ x.w;
+            }
+        }
+    }
+    const int64_t g = (int64_t)blockIdx.x * kDynWaves + wave;
     if (acc == 0x9E3779B9u) sink[g * 64 + lane] = acc;
 }
 
@@ -207,6 +252,24 @@ int ceil_read3(const float* a, const float* b, const float* c, int64_t n, int32_
     const dim3 grid((unsigned)(cus_of_current() * blocks_per_cu));
     hipLaunchKernelGGL(read3_kernel, grid, dim3(kBlock), 0, (hipStream_t)stream, a, b, c, tiles,
                        sink);
+    return hipGetLastError() == hipSuccess ? 0 : 4;
+}
+
+// ceil_read3 with the dynamic split of read3_dynamic_kernel: one block of
+// 12 waves per CU; counter: device uint64, zero on entry (the call leaves
+// it at the number of chunks taken); sink: device uint32[64 *
+// ceil_read3_waves(3)].  Returns 0, 1 on a bad argument, 4 on a HIP error.
+int ceil_read3_dynamic(const float* a, const float* b, const float* c, int64_t n,
+                       unsigned long long* counter, uint32_t* sink, void* stream)
+{
+    if (!a || !b || !c || !sink || !counter || n < 0 ||
+        ((reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b) |
+          reinterpret_cast<uintptr_t>(c)) & 15u) != 0)
+        return 1;
+    const int64_t tiles = n / kTile;
+    if (tiles == 0) return 0;
+    hipLaunchKernelGGL(read3_dynamic_kernel, dim3((unsigned)cus_of_current()),
+                       dim3(64 * kDynWaves), 0, (hipStream_t)stream, a, b, c, tiles, counter, sink);
     return hipGetLastError() == hipSuccess ? 0 : 4;
 }
 

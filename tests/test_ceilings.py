@@ -21,6 +21,8 @@ def lib():
     L.ceil_read3_waves.argtypes = [I32]
     L.ceil_read3.restype = ctypes.c_int
     L.ceil_read3.argtypes = [P, P, P, I64, I32, P, P]
+    L.ceil_read3_dynamic.restype = ctypes.c_int
+    L.ceil_read3_dynamic.argtypes = [P, P, P, I64, P, P, P]
     L.ceil_read3_write.restype = ctypes.c_int
     L.ceil_read3_write.argtypes = [P, P, P, I64, I64, P, P, I32, P, P]
     L.ceil_write_entries.restype = ctypes.c_int
@@ -37,6 +39,9 @@ def test_bad_arguments_are_refused_before_device_work():
     assert L.ceil_read3(fake, fake, fake, -1, 3, fake, None) == 1
     assert L.ceil_read3(fake + 4, fake, fake, 1 << 20, 3, fake, None) == 1     # misaligned
     assert L.ceil_read3(fake, fake, fake, 1 << 20, 0, fake, None) == 1
+    assert L.ceil_read3_dynamic(fake, fake, fake, 1 << 20, None, fake, None) == 1
+    assert L.ceil_read3_dynamic(fake, fake + 8, fake, 1 << 20, fake, fake, None) == 1
+    assert L.ceil_read3_dynamic(fake, fake, fake, -1, fake, fake, None) == 1
     assert L.ceil_read3_write(fake, fake, fake, 1 << 20, 10, None, fake, 3, fake, None) == 1
     assert L.ceil_read3_write(fake, fake, fake, 1 << 20, -1, fake, fake, 3, fake, None) == 1
     assert L.ceil_read3_write(fake, fake, fake, 1 << 20, 10, fake + 4, fake, 3, fake, None) == 1
@@ -62,6 +67,14 @@ def test_reference_kernels_write_what_they_state():
     sink = torch.zeros(64 * L.ceil_read3_waves(3), dtype=torch.int32, device="cuda")
     assert L.ceil_read3(a.data_ptr(), b.data_ptr(), c.data_ptr(), n, 3, sink.data_ptr(),
                         s.cuda_stream) == 0
+    counter = torch.zeros(1, dtype=torch.int64, device="cuda")
+    assert L.ceil_read3_dynamic(a.data_ptr(), b.data_ptr(), c.data_ptr(), n, counter.data_ptr(),
+                                sink.data_ptr(), s.cuda_stream) == 0
+    torch.cuda.synchronize()
+    # every block takes chunks of 48 tiles until one starts past the end
+    chunks = -(-(n // TILE) // 48)
+    blocks = torch.cuda.get_device_properties(0).multi_processor_count
+    assert int(counter.item()) == chunks + blocks
     tiles, e = n // TILE, 1001
     idx = torch.full((e + 8,), -7, dtype=torch.int64, device="cuda")
     val = torch.full((e + 8,), 7, dtype=torch.int16, device="cuda")

@@ -35,16 +35,19 @@
 //    before it) plus its own selected predecessors in the lane, so
 //    candidates are queued, and changed entries (packed 32-bit position +
 //    BF16 value) staged in LDS, in ascending element order: every wave's
-//    output is ascending.  A wave reserves global output space with one
-//    atomicAdd on the 64-bit cursor per flush of its staging area, always
-//    exactly 1024 entries except a wave's last flush (so the output is made
-//    of whole 1024-entry runs, each ascending, until the waves finish), then
-//    writes the entries out coalesced; in the unordered call the waves of a
-//    block combine their reservations (block_round below);
-//  - ordered mode: each flush also records (unordered position, entries of
-//    the wave before it, count, wave) and each wave its total; a scan of the
-//    wave totals and a copy of the recorded runs then give the entries in
-//    ascending offset order (order_kernel below), deterministic whatever
+//    output is ascending.  In the unordered call the waves of a block meet
+//    every four tiles and, once they hold enough entries, reserve output
+//    space for all of them with one atomicAdd on the 64-bit cursor
+//    (block_round below); each wave writes its run after those of the waves
+//    before it, coalesced.  A wave whose staging area (kWaveStage entries)
+//    fills between two meetings flushes exactly kWaveStage entries on its
+//    own with one atomicAdd;
+//  - ordered mode: each wave writes its flushes to a region of the
+//    workspace of its own (no atomics) and, once that is full, to a shared
+//    area, recording (position, entries of the wave before it, count,
+//    wave); a scan of the wave totals and a copy of the regions and
+//    recorded runs then give the entries in ascending offset order
+//    (order_scan_kernel, order_copy_kernel below), deterministic whatever
 //    the timing of the atomics.
 #include <hip/hip_runtime.h>
 

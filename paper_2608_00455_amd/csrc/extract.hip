@@ -42,8 +42,10 @@
 //    before it, coalesced.  A wave whose staging area (kWaveStage entries)
 //    fills between two meetings flushes exactly kWaveStage entries on its
 //    own with one atomicAdd;
-//  - ordered mode: each wave writes its flushes to a region of the
-//    workspace of its own (no atomics) and, once that is full, to a shared
+//  - ordered mode: the waves of a block still meet every four tiles (a
+//    barrier alone), which keeps them in step; each wave writes its
+//    flushes to a region of the workspace of its own (no atomics) and,
+//    once that is full, to a shared
 //    area, recording (position, entries of the wave before it, count,
 //    wave); a scan of the wave totals and a copy of the regions and
 //    recorded runs then give the entries in ascending offset order
@@ -642,8 +644,12 @@ __global__ __launch_bounds__(64 * kWavesOf<kFull>) void extract_kernel(ExtractPa
             process_tile<kFull, kVecLoads, kDecayOne, kWritePrev, kLit, kRoute>(
                 a, t * kWaveTile, lane, so, queued, st, (uint32_t)it, P, M, V);
         }
-        if (combine && it % kRound == kRound - 1)
-            block_round(a, st, so, lane, wave, s_cnt, s_base, (round++) & 1, false);
+        if (it % kRound == kRound - 1) {
+            if (combine)
+                block_round(a, st, so, lane, wave, s_cnt, s_base, (round++) & 1, false);
+            else if (!kRoute)
+                __syncthreads();   // ordered: keeps the block's waves in step
+        }
     }
     if (queued > 0) drain_queue<kDecayOne, kLit, kRoute>(a, st, queued, so, lane);
     if (kTail && tail > 0) {

@@ -158,7 +158,7 @@ def ceilings(p, m, v, pipe, stream, entries, reps=5, touch=None):
         ms = timed(lambda: lib.ceil_read3(p.data_ptr(), m.data_ptr(), v.data_ptr(), n, bpc,
                                           sink.data_ptr(), s), "ceil_read3")
         if best is None or ms < best[0]:
-            best = (ms, bpc)
+            best = (ms, "static", bpc, 4)
         del sink
     sink = torch.zeros(64 * lib.ceil_read3_waves(3), dtype=torch.int32, device="cuda")
     counter = torch.zeros(1, dtype=torch.int64, device="cuda")
@@ -169,10 +169,11 @@ def ceilings(p, m, v, pipe, stream, entries, reps=5, touch=None):
                                       counter.data_ptr(), sink.data_ptr(), s)
     ms = timed(dynamic_read, "ceil_read3_dynamic")
     if ms < best[0]:
-        best = (ms, "12-wave block, dynamic split")
+        best = (ms, "dynamic", 1, 12)
     del sink, counter
     out["read_stream"] = {"gbs": 12 * n / (best[0] / 1e3) / 1e9, "ms": best[0],
-                          "blocks_per_cu": best[1], "bytes": 12 * n}
+                          "split": best[1], "blocks_per_cu": best[2],
+                          "waves_per_block": best[3], "bytes": 12 * n}
     e = min(entries, pipe.capacity)
     if e > 0:
         rd = best[0]

@@ -724,3 +724,21 @@ def test_unordered_tail_taken_in_chunks(case):
     got_i = got_i[5:5 + want_idx.size]
     order = np.argsort(got_i)
     assert np.array_equal(got_i[order], want_idx) and np.array_equal(got_v[order], want_val)
+    if case == "partial":
+        # a second call appending to the same cursor (the next range of a
+        # shard with the same data) starts from a cleared cursor
+        idx2 = torch.full((2 * cap,), -1, dtype=torch.int64, device="cuda")
+        val2 = torch.zeros(2 * cap, dtype=torch.int16, device="cuda")
+        cursor.fill_(0)
+        for base in (100, 100 + n):
+            B.dte_extract_delta(dp.data_ptr(), dm.data_ptr(), dv.data_ptr(), n, base, hp,
+                                idx2.data_ptr(), val2.data_ptr(), 2 * cap, cursor.data_ptr(), 0,
+                                torch.cuda.current_stream().cuda_stream)
+        sync()
+        k = want_idx.size
+        assert int(cursor.item()) == 2 * k
+        got_i = idx2.cpu().numpy()[:2 * k]
+        got_v = val2.cpu().numpy().view(np.uint16)[:2 * k]
+        order = np.argsort(got_i)
+        assert np.array_equal(got_i[order], np.concatenate([want_idx, want_idx + n]))
+        assert np.array_equal(got_v[order], np.concatenate([want_val, want_val]))
